@@ -1,0 +1,251 @@
+/*
+ * amk.h -- C ABI of the batch-1 Llama decode megakernel for MI355X (gfx950).
+ *
+ * One call of amk_decode_step() runs one forward pass of a Llama-family
+ * decoder for one token as ONE persistent cooperative kernel launch, and
+ * leaves the greedy next token on the device (paper §3, Figure fig:pipeline:
+ * one launch = one forward pass = one token).  Work is split into tasks that
+ * the host lowers into per-CU queues (paper §3 Layer 0 and Algorithm alg:sm);
+ * tasks on different CUs order themselves only through monotonic counters
+ * that producers increment with release semantics and consumers wait on with
+ * acquire semantics (paper §4 "Synchronization model").  Before anything is
+ * launched the host checks the schedule (paper §4 "The invariants validate()
+ * proves", Table tab:checks); a rejected schedule is never launched.
+ *
+ * Model family (paper §6 "Architecture coverage"): bias-free projections,
+ * full-rotary RoPE (rotate-half pairs i, i + head_dim/2), SiLU-SwiGLU MLP,
+ * RMSNorm, grouped-query attention.  Weight formats (paper §5 "Quantized
+ * generation"): bf16, or W8A16 = int8 weights with one fp32 scale per output
+ * row (symmetric, dequantisation folded into the GEMV).  Activations are fp32
+ * throughout; the KV cache is bf16.
+ *
+ * Conventions for every function:
+ *   - returns an int status (AMK_OK or a negative AMK_ERR_*), never throws or
+ *     aborts across the ABI;
+ *   - "device pointer" means memory of the device the handle was created on
+ *     (hipMalloc or torch allocations); "host pointer" means ordinary memory;
+ *   - nothing here frees or copies caller memory.
+ *
+ * Plain C; callers need no HIP headers.  The stream argument is a hipStream_t
+ * passed as void* (NULL = the null stream).
+ */
+#ifndef AMK_H_
+#define AMK_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AMK_ABI_VERSION 1
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+  AMK_OK = 0,
+  AMK_ERR_INVALID_ARGUMENT = -1,      /* NULL pointer, out-of-range token / pos, bad enum */
+  AMK_ERR_UNSUPPORTED = -2,           /* shape or alignment outside the supported family */
+  AMK_ERR_SCHEDULE_REJECTED = -3,     /* the static schedule check failed: nothing launched */
+  AMK_ERR_OUT_OF_MEMORY = -4,
+  AMK_ERR_DEVICE = -5,                /* a HIP runtime call failed */
+  AMK_ERR_COOPERATIVE_UNSUPPORTED = -6, /* no cooperative launch, or too few co-resident workgroups */
+  AMK_ERR_TIMEOUT = -7,               /* a device-side counter wait exceeded its deadline (sticky) */
+  AMK_ERR_BAD_STATE = -8,             /* handle in an error state; call amk_reset() */
+  AMK_ERR_ABORTED = -9                /* the host abort flag stopped a launch (sticky) */
+};
+
+enum { AMK_WEIGHTS_BF16 = 0, AMK_WEIGHTS_W8A16 = 1 };
+
+/* ---- model description ------------------------------------------------- */
+typedef struct {
+  uint32_t abi_version;     /* must be AMK_ABI_VERSION */
+  int32_t hidden;           /* H; H, intermediate and n_heads * head_dim are multiples of 16 */
+  int32_t n_layers;         /* L */
+  int32_t n_heads;          /* query heads */
+  int32_t n_kv_heads;       /* KV heads; n_heads % n_kv_heads == 0, n_heads / n_kv_heads <= 8 */
+  int32_t head_dim;         /* d; a power of two in [64, 256] */
+  int32_t intermediate;     /* SwiGLU width I */
+  int32_t vocab;            /* V */
+  int32_t max_seq;          /* KV cache capacity in positions */
+  float rope_theta;
+  float rms_eps;
+  int32_t tied_embeddings;  /* 1: the LM head is the embedding table (stays bf16) */
+  int32_t weight_format;    /* AMK_WEIGHTS_BF16 or AMK_WEIGHTS_W8A16 */
+  int32_t device;           /* HIP device ordinal; -1 = current device */
+} amk_config_t;
+
+/* One projection y = W x.  w: device pointer to a row-major [out, in] matrix
+ * (nn.Linear layout), bf16 or int8 per the config; scale: device pointer to
+ * fp32[out] for int8 weights, NULL for bf16.  16-byte aligned. */
+typedef struct {
+  const void* w;
+  const float* scale;
+} amk_linear_t;
+
+typedef struct {
+  const void* attn_norm;  /* bf16 [H] */
+  const void* mlp_norm;   /* bf16 [H] */
+  amk_linear_t q;         /* [n_heads * d, H] */
+  amk_linear_t k;         /* [n_kv_heads * d, H] */
+  amk_linear_t v;         /* [n_kv_heads * d, H] */
+  amk_linear_t o;         /* [H, n_heads * d] */
+  amk_linear_t gate;      /* [I, H] */
+  amk_linear_t up;        /* [I, H] */
+  amk_linear_t down;      /* [H, I] */
+} amk_layer_weights_t;
+
+typedef struct {
+  const void* embed;                 /* bf16 [V, H] device pointer */
+  const void* final_norm;            /* bf16 [H] */
+  amk_linear_t lm_head;              /* untied: [V, H] (int8 + scale under W8A16); tied: w = NULL */
+  const amk_layer_weights_t* layers; /* HOST array [n_layers] of device pointers; read during amk_create only */
+} amk_weights_t;
+
+/* Optional tuning; zero fields take defaults. */
+typedef struct {
+  int32_t attn_splits;      /* attention tasks per KV head (1..64); 0 = derived from the CU count */
+  int32_t timeout_us;       /* deadline of one device counter wait in microseconds; 0 = 2 s */
+  int32_t max_rows_per_task;/* cap on rows of one GEMV task; 0 = 1024 */
+} amk_tuning_t;
+
+typedef struct amk_handle_s* amk_handle_t;
+
+/* ---- lifecycle ----------------------------------------------------------- */
+
+/* Validate the config and weight pointers, build the per-CU task schedule for
+ * the device, check it (acyclic, wait-satisfiable, deadlock-free queue order,
+ * race-free reads and writes, every output produced exactly once), and upload
+ * the schedule tables, counters, scratch activations and the RoPE table.
+ * Weight pointers are BORROWED: they must stay valid and unchanged until
+ * amk_destroy(); nothing is copied or repacked.  tuning may be NULL.
+ * On failure *out is set to NULL and nothing stays allocated. */
+int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
+               amk_handle_t* out);
+
+/* Enqueue one decode step on `stream` (asynchronous: returns before the GPU
+ * finishes).  Reads token `token` at position `pos`, reads KV positions
+ * 0..pos-1 and appends position pos (all layers), writes all `vocab` logits
+ * and the greedy next token (lowest index among equal maxima) into the
+ * handle's device slot (amk_next_token_ptr).
+ *   kv_cache: device pointer, bf16 [n_layers][2 (K, V)][n_kv_heads][max_seq][head_dim]
+ *   logits:   device pointer, fp32 [vocab]
+ * Errors: AMK_ERR_INVALID_ARGUMENT for token outside [0, vocab) or pos outside
+ * [0, max_seq); a sticky device error of an earlier step (AMK_ERR_TIMEOUT /
+ * AMK_ERR_ABORTED, visible once that step finished) is returned and nothing
+ * is launched until amk_reset().  One handle must not be driven from two
+ * streams at once. */
+int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, float* logits,
+                    void* stream);
+
+/* Synchronise the device, free everything the handle owns.  NULL is a no-op. */
+int amk_destroy(amk_handle_t h);
+
+/* ---- helpers --------------------------------------------------------------- */
+
+/* Bytes of the KV cache amk_decode_step expects for cfg (0 for an invalid cfg). */
+size_t amk_kv_cache_bytes(const amk_config_t* cfg);
+
+/* Device pointer to the int32 next-token slot written by every step. */
+const int32_t* amk_next_token_ptr(amk_handle_t h);
+
+/* Copy the next token written by the last enqueued step into *dst (host
+ * memory): enqueues the copy on `stream` and waits for it. */
+int amk_copy_next_token(amk_handle_t h, int32_t* dst, void* stream);
+
+/* Synchronise the handle's last stream and return its sticky device status
+ * (AMK_OK, AMK_ERR_TIMEOUT, AMK_ERR_ABORTED). */
+int amk_get_status(amk_handle_t h);
+
+/* Clear a sticky error: waits for the device, zeroes the counters and
+ * restarts the epoch.  The KV cache content is the caller's business. */
+int amk_reset(amk_handle_t h);
+
+/* Raise (value 1) or clear (value 0) the host abort flag.  A launch whose
+ * workgroup is spinning on a counter polls the flag about every hundred spins
+ * and, once it sees it, stops every workgroup and records AMK_ERR_ABORTED
+ * (sticky).  The flag lives in host-mapped memory, so it can be raised while
+ * a step runs. */
+int amk_set_abort(amk_handle_t h, int32_t value);
+
+const char* amk_status_string(int status);
+
+/* ---- schedule introspection (CPU only, no device needed) -------------------- */
+
+/* Operations of the task graph, in the order of one layer. */
+enum {
+  AMK_OP_QKV = 1,      /* RMSNorm + q/k/v GEMV of RoPE row-pair units [begin, end) + RoPE + KV append */
+  AMK_OP_ATTN = 2,     /* partial attention of KV head `aux`, position split `begin` of `end` */
+  AMK_OP_COMBINE = 3,  /* merge the position splits of query heads [begin, end) */
+  AMK_OP_O = 4,        /* rows [begin, end) of x1 = x + Wo o */
+  AMK_OP_GATEUP = 5,   /* rows [begin, end) of a = silu(Wg h2) * (Wu h2), h2 = RMSNorm(x1) */
+  AMK_OP_DOWN = 6,     /* rows [begin, end) of x2 = x1 + Wd a */
+  AMK_OP_LMHEAD = 7,   /* rows [begin, end) of logits = W_lm RMSNorm(x); argmax partial slot `aux` */
+  AMK_OP_ARGMAX = 8    /* reduce argmax partial slots [begin, end) into the next token */
+};
+
+#define AMK_MAX_WAITS 4
+
+/* Fixed-size task descriptor (64 bytes), the unit the device walks.  A task
+ * waits until, for every i < n_wait, counter wait_counter[i] has been
+ * incremented wait_count[i] times in this launch, then runs, then increments
+ * signal_counter (if >= 0) once. */
+typedef struct {
+  uint16_t op;
+  uint16_t layer;
+  int32_t cu;          /* queue (workgroup index) that runs the task */
+  int32_t seq;         /* position inside that queue, 0-based, contiguous */
+  int32_t begin, end;  /* op-specific range, see AMK_OP_* */
+  int32_t aux;         /* op-specific */
+  int32_t n_wait;
+  int32_t wait_counter[AMK_MAX_WAITS];
+  int32_t wait_count[AMK_MAX_WAITS];
+  int32_t signal_counter;
+} amk_task_t;
+
+typedef struct {
+  int32_t ok;            /* 1 accepted, 0 rejected */
+  int32_t rule;          /* first failed rule, AMK_CHECK_* */
+  int32_t task;          /* offending task index (or -1) */
+  int32_t other;         /* second task / counter involved (or -1) */
+  int32_t n_tasks, n_counters, n_edges;
+  char message[256];
+} amk_check_report_t;
+
+enum {
+  AMK_CHECK_OK = 0,
+  AMK_CHECK_WELL_FORMED = 1,   /* bad op, counter index, queue index, range or arity */
+  AMK_CHECK_CAPACITY = 2,      /* more waits than AMK_MAX_WAITS, rows over the LDS budget */
+  AMK_CHECK_WAIT_SATISFIABLE = 3, /* count < 1, counter without producer, count > producers */
+  AMK_CHECK_ALL_JOIN = 4,      /* a multi-producer counter waited on with count != producers */
+  AMK_CHECK_ACYCLIC = 5,       /* cycle in producer->consumer edges plus per-queue order edges */
+  AMK_CHECK_QUEUE_ORDER = 6,   /* a consumer queued before its producer on the same CU */
+  AMK_CHECK_RACE = 7,          /* a read not ordered after every writer of the region it reads */
+  AMK_CHECK_KV_ORDER = 8,      /* a KV-cache read not ordered after this pass's append */
+  AMK_CHECK_OUTPUT = 9         /* an output region written twice or never */
+};
+
+/* Number of tasks / counters the schedule of cfg has on n_cu queues (after
+ * validating cfg; tuning may be NULL).  Returns a status. */
+int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu,
+                      int32_t* n_tasks, int32_t* n_counters);
+
+/* Lower cfg onto n_cu queues into tasks[cap] (cap >= n_tasks). */
+int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu,
+                        amk_task_t* tasks, int32_t cap, int32_t* n_tasks, int32_t* n_counters);
+
+/* Check an arbitrary task array for cfg on n_cu queues with n_counters
+ * counters.  Never fails for a bad schedule: the verdict is in *report
+ * (report->ok); the return value is AMK_OK unless the arguments themselves
+ * are unusable.  Accepted iff amk_create would launch it. */
+int amk_schedule_check(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu,
+                       const amk_task_t* tasks, int32_t n_tasks, int32_t n_counters,
+                       amk_check_report_t* report);
+
+/* Validate cfg and build + check its schedule for n_cu queues (no device). */
+int amk_check_config(const amk_config_t* cfg, int32_t n_cu);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AMK_H_ */

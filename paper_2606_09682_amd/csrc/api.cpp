@@ -1,0 +1,438 @@
+// C ABI of the decode megakernel: handle lifecycle, launch, schedule
+// introspection.  Host code only; the kernel lives in megakernel.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/amk.h"
+#include "device.h"
+#include "schedule.h"
+
+using amk::DevLayer;
+using amk::DevModel;
+using amk::Schedule;
+using amk::Shape;
+using amk::amk_internal_attn_scratch;
+using amk::amk_internal_launch;
+using amk::amk_internal_occupancy;
+using amk::amk_internal_prepare;
+using amk::amk_internal_threads;
+
+struct amk_handle_s {
+  Shape s;
+  int device = 0;
+  Schedule sch;
+  DevModel dm;
+  void* d_block = nullptr;      // one device allocation for tables and scratch
+  int32_t* h_status = nullptr;  // host-mapped
+  int32_t* h_abort = nullptr;   // host-mapped
+  uint32_t epoch = 0;
+  void* last_stream = nullptr;
+  bool launched = false;
+  uint64_t timeout_ticks = 0;
+};
+
+namespace {
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) return;
+    ok = dev < 0 || dev == prev || hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_linear(const amk_linear_t& l, bool int8) {
+  if (!l.w || !aligned16(l.w)) return AMK_ERR_INVALID_ARGUMENT;
+  if (int8 && (!l.scale || ((uintptr_t)l.scale & 3u))) return AMK_ERR_INVALID_ARGUMENT;
+  return AMK_OK;
+}
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+void free_handle(amk_handle_s* h) {
+  if (!h) return;
+  DeviceGuard g(h->device);
+  if (h->launched) (void)hipDeviceSynchronize();
+  if (h->d_block) (void)hipFree(h->d_block);
+  if (h->h_status) (void)hipHostFree(h->h_status);
+  if (h->h_abort) (void)hipHostFree(h->h_abort);
+  delete h;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* amk_status_string(int status) {
+  switch (status) {
+    case AMK_OK: return "ok";
+    case AMK_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case AMK_ERR_UNSUPPORTED: return "unsupported model shape or layout";
+    case AMK_ERR_SCHEDULE_REJECTED: return "schedule rejected by the static check";
+    case AMK_ERR_OUT_OF_MEMORY: return "out of device or host memory";
+    case AMK_ERR_DEVICE: return "HIP runtime error";
+    case AMK_ERR_COOPERATIVE_UNSUPPORTED: return "cooperative launch unavailable or too few co-resident workgroups";
+    case AMK_ERR_TIMEOUT: return "device counter wait timed out";
+    case AMK_ERR_BAD_STATE: return "handle in an error state";
+    case AMK_ERR_ABORTED: return "launch aborted by the host abort flag";
+    default: return "unknown status";
+  }
+}
+
+size_t amk_kv_cache_bytes(const amk_config_t* cfg) {
+  Shape s;
+  if (amk::derive_shape(cfg, nullptr, 1, &s, nullptr) != AMK_OK) return 0;
+  return (size_t)s.L * 2 * s.nkv * (size_t)s.max_seq * s.hd * 2;
+}
+
+int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t* n_tasks,
+                      int32_t* n_counters) {
+  try {
+    Shape s;
+    int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
+    if (st != AMK_OK) return st;
+    Schedule sch = amk::build_schedule(s, n_cu);
+    if (n_tasks) *n_tasks = (int32_t)sch.tasks.size();
+    if (n_counters) *n_counters = sch.n_counters;
+    return AMK_OK;
+  } catch (const std::bad_alloc&) {
+    return AMK_ERR_OUT_OF_MEMORY;
+  } catch (...) {
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+}
+
+int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, amk_task_t* tasks,
+                        int32_t cap, int32_t* n_tasks, int32_t* n_counters) {
+  try {
+    Shape s;
+    int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
+    if (st != AMK_OK) return st;
+    Schedule sch = amk::build_schedule(s, n_cu);
+    if (n_tasks) *n_tasks = (int32_t)sch.tasks.size();
+    if (n_counters) *n_counters = sch.n_counters;
+    if (!tasks || cap < (int32_t)sch.tasks.size()) return AMK_ERR_INVALID_ARGUMENT;
+    std::memcpy(tasks, sch.tasks.data(), sch.tasks.size() * sizeof(amk_task_t));
+    return AMK_OK;
+  } catch (const std::bad_alloc&) {
+    return AMK_ERR_OUT_OF_MEMORY;
+  } catch (...) {
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+}
+
+int amk_schedule_check(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, const amk_task_t* tasks,
+                       int32_t n_tasks, int32_t n_counters, amk_check_report_t* report) {
+  if (!report) return AMK_ERR_INVALID_ARGUMENT;
+  try {
+    Shape s;
+    int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
+    if (st != AMK_OK) return st;
+    amk::check_schedule(s, n_cu, tasks, n_tasks, n_counters, report);
+    return AMK_OK;
+  } catch (const std::bad_alloc&) {
+    return AMK_ERR_OUT_OF_MEMORY;
+  } catch (...) {
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+}
+
+int amk_check_config(const amk_config_t* cfg, int32_t n_cu) {
+  try {
+    Shape s;
+    int st = amk::derive_shape(cfg, nullptr, n_cu, &s, nullptr);
+    if (st != AMK_OK) return st;
+    Schedule sch = amk::build_schedule(s, n_cu);
+    amk_check_report_t rep;
+    if (!amk::check_schedule(s, n_cu, sch.tasks.data(), (int)sch.tasks.size(), sch.n_counters, &rep))
+      return AMK_ERR_SCHEDULE_REJECTED;
+    return AMK_OK;
+  } catch (const std::bad_alloc&) {
+    return AMK_ERR_OUT_OF_MEMORY;
+  } catch (...) {
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+}
+
+int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning, amk_handle_t* out) {
+  if (!out) return AMK_ERR_INVALID_ARGUMENT;
+  *out = nullptr;
+  if (!cfg || !w) return AMK_ERR_INVALID_ARGUMENT;
+  amk_handle_s* h = nullptr;
+  try {
+    DeviceGuard guard(cfg->device);
+    if (!guard.ok) return AMK_ERR_DEVICE;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return AMK_ERR_DEVICE;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return AMK_ERR_DEVICE;
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return AMK_ERR_UNSUPPORTED;
+    int coop = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop)
+      return AMK_ERR_COOPERATIVE_UNSUPPORTED;
+    const int n_cu = prop.multiProcessorCount;
+
+    Shape s;
+    std::string why;
+    int st = amk::derive_shape(cfg, tuning, n_cu, &s, &why);
+    if (st != AMK_OK) return st;
+
+    // weights: presence, alignment, format
+    const bool q8 = s.fmt == AMK_WEIGHTS_W8A16;
+    if (!w->embed || !aligned16(w->embed) || !w->final_norm || !aligned16(w->final_norm) || !w->layers)
+      return AMK_ERR_INVALID_ARGUMENT;
+    if (s.tied) {
+      if (w->lm_head.w) return AMK_ERR_INVALID_ARGUMENT;
+    } else if (check_linear(w->lm_head, q8) != AMK_OK) {
+      return AMK_ERR_INVALID_ARGUMENT;
+    }
+    for (int l = 0; l < s.L; ++l) {
+      const amk_layer_weights_t& lw = w->layers[l];
+      if (!lw.attn_norm || !aligned16(lw.attn_norm) || !lw.mlp_norm || !aligned16(lw.mlp_norm))
+        return AMK_ERR_INVALID_ARGUMENT;
+      const amk_linear_t* ls[7] = {&lw.q, &lw.k, &lw.v, &lw.o, &lw.gate, &lw.up, &lw.down};
+      for (auto* lp : ls)
+        if (check_linear(*lp, q8) != AMK_OK) return AMK_ERR_INVALID_ARGUMENT;
+    }
+
+    h = new amk_handle_s();
+    h->s = s;
+    h->device = dev;
+    h->sch = amk::build_schedule(s, n_cu);
+    amk_check_report_t rep;
+    if (!amk::check_schedule(s, n_cu, h->sch.tasks.data(), (int)h->sch.tasks.size(), h->sch.n_counters, &rep)) {
+      std::fprintf(stderr, "amk: schedule rejected (rule %d): %s\n", rep.rule, rep.message);
+      free_handle(h);
+      return AMK_ERR_SCHEDULE_REJECTED;
+    }
+
+    // LDS: activation vector (padded to a whole int8 granule) + partials / attention scratch
+    const int nsw = amk_internal_threads() / 64 - 1;
+    const size_t act = round_up((size_t)std::max({s.H, s.nq * s.hd, s.I}), 1024);
+    const size_t scr = std::max<size_t>((size_t)nsw * s.max_jobs, (size_t)amk_internal_attn_scratch(s.group, s.hd));
+    const size_t lds_bytes = (act + scr) * 4;
+    int max_lds = 0;
+    if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+      free_handle(h);
+      return AMK_ERR_DEVICE;
+    }
+    if ((long)lds_bytes + 256 > (long)max_lds) {
+      std::fprintf(stderr, "amk: needs %zu B of LDS per workgroup, device allows %d\n", lds_bytes, max_lds);
+      free_handle(h);
+      return AMK_ERR_UNSUPPORTED;
+    }
+    if (amk_internal_prepare(s.group, (int)lds_bytes) != AMK_OK) {
+      free_handle(h);
+      return AMK_ERR_DEVICE;
+    }
+    int per_cu = 0;
+    if (amk_internal_occupancy(s.group, (int)lds_bytes, &per_cu) != AMK_OK || per_cu < 1) {
+      free_handle(h);
+      return AMK_ERR_COOPERATIVE_UNSUPPORTED;
+    }
+
+    // device block layout
+    const int L = s.L;
+    const int n_lm = h->sch.n_lm_slots;
+    const int rec = s.group * (amk::kPartHead + s.hd);
+    struct Region { size_t off, bytes; };
+    size_t top = 0;
+    auto take = [&](size_t bytes) { Region r{top, bytes}; top = round_up(top + bytes, 256); return r; };
+    const Region r_layers = take(sizeof(DevLayer) * L);
+    const Region r_rope = take(sizeof(float) * 2 * (size_t)s.max_seq * s.half);
+    const Region r_x = take(sizeof(float) * (size_t)(2 * L + 1) * s.H);
+    const Region r_q = take(sizeof(float) * (size_t)L * s.nq * s.hd);
+    const Region r_part = take(sizeof(float) * (size_t)L * s.nkv * s.nsplit * rec);
+    const Region r_o = take(sizeof(float) * (size_t)L * s.nq * s.hd);
+    const Region r_a = take(sizeof(float) * (size_t)L * s.I);
+    const Region r_argp = take(sizeof(float) * 2 * n_lm);
+    const Region r_next = take(sizeof(int32_t));
+    const Region r_ctr = take(sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch.n_counters);
+    const Region r_abort = take(sizeof(int32_t));
+    const Region r_tasks = take(sizeof(amk_task_t) * h->sch.tasks.size());
+    const Region r_queue = take(sizeof(int32_t) * h->sch.queue_start.size());
+    if (hipMalloc(&h->d_block, top) != hipSuccess) {
+      h->d_block = nullptr;
+      free_handle(h);
+      return AMK_ERR_OUT_OF_MEMORY;
+    }
+    char* base = (char*)h->d_block;
+    if (hipMemset(h->d_block, 0, top) != hipSuccess) {
+      free_handle(h);
+      return AMK_ERR_DEVICE;
+    }
+    if (hipHostMalloc((void**)&h->h_status, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+            hipSuccess ||
+        hipHostMalloc((void**)&h->h_abort, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+            hipSuccess) {
+      free_handle(h);
+      return AMK_ERR_OUT_OF_MEMORY;
+    }
+    *(volatile int32_t*)h->h_status = 0;
+    *(volatile int32_t*)h->h_abort = 0;
+    int32_t* d_status = nullptr;
+    int32_t* d_hab = nullptr;
+    if (hipHostGetDevicePointer((void**)&d_status, h->h_status, 0) != hipSuccess ||
+        hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess) {
+      free_handle(h);
+      return AMK_ERR_DEVICE;
+    }
+
+    // host-built tables
+    std::vector<DevLayer> layers(L);
+    for (int l = 0; l < L; ++l) {
+      const amk_layer_weights_t& lw = w->layers[l];
+      const amk_linear_t* ls[7] = {&lw.q, &lw.k, &lw.v, &lw.o, &lw.gate, &lw.up, &lw.down};
+      for (int i = 0; i < 7; ++i) {
+        layers[l].w[i] = ls[i]->w;
+        layers[l].s[i] = q8 ? ls[i]->scale : nullptr;
+      }
+      layers[l].attn_norm = (const uint16_t*)lw.attn_norm;
+      layers[l].mlp_norm = (const uint16_t*)lw.mlp_norm;
+    }
+    // RoPE table: angle p * theta^(-2i/d), cos and sin evaluated in float64, stored float32
+    std::vector<float> rope(2 * (size_t)s.max_seq * s.half);
+    for (int i = 0; i < s.half; ++i) {
+      const double inv = std::pow((double)s.theta, -2.0 * i / (double)s.hd);
+      for (int p = 0; p < s.max_seq; ++p) {
+        const double a = (double)p * inv;
+        rope[2 * ((size_t)p * s.half + i)] = (float)std::cos(a);
+        rope[2 * ((size_t)p * s.half + i) + 1] = (float)std::sin(a);
+      }
+    }
+    bool ok = hipMemcpy(base + r_layers.off, layers.data(), r_layers.bytes, hipMemcpyHostToDevice) == hipSuccess &&
+              hipMemcpy(base + r_rope.off, rope.data(), r_rope.bytes, hipMemcpyHostToDevice) == hipSuccess &&
+              hipMemcpy(base + r_tasks.off, h->sch.tasks.data(), r_tasks.bytes, hipMemcpyHostToDevice) ==
+                  hipSuccess &&
+              hipMemcpy(base + r_queue.off, h->sch.queue_start.data(), r_queue.bytes, hipMemcpyHostToDevice) ==
+                  hipSuccess;
+    if (!ok) {
+      free_handle(h);
+      return AMK_ERR_DEVICE;
+    }
+
+    DevModel& m = h->dm;
+    std::memset(&m, 0, sizeof(m));
+    m.H = s.H; m.L = L; m.nq = s.nq; m.nkv = s.nkv; m.hd = s.hd; m.I = s.I; m.V = s.V; m.max_seq = s.max_seq;
+    m.fmt = s.fmt;
+    m.lm_int8 = q8 && !s.tied;
+    m.group = s.group; m.half = s.half;
+    m.half_log2 = 0;
+    while ((1 << m.half_log2) < s.half) ++m.half_log2;
+    m.units = s.units; m.q_units = s.q_units; m.nsplit = s.nsplit; m.n_lm = n_lm;
+    m.n_cu = n_cu;
+    m.eps = s.eps;
+    m.attn_scale = (float)(1.0 / std::sqrt((double)s.hd));
+    m.embed = (const uint16_t*)w->embed;
+    m.final_norm = (const uint16_t*)w->final_norm;
+    m.lm_w = s.tied ? w->embed : w->lm_head.w;
+    m.lm_s = m.lm_int8 ? w->lm_head.scale : nullptr;
+    m.layers = (const DevLayer*)(base + r_layers.off);
+    m.rope = (const float2*)(base + r_rope.off);
+    m.x = (float*)(base + r_x.off);
+    m.q = (float*)(base + r_q.off);
+    m.part = (float*)(base + r_part.off);
+    m.o = (float*)(base + r_o.off);
+    m.a = (float*)(base + r_a.off);
+    m.argp = (float*)(base + r_argp.off);
+    m.next_token = (int32_t*)(base + r_next.off);
+    m.counters = (uint32_t*)(base + r_ctr.off);
+    m.dev_abort = (int32_t*)(base + r_abort.off);
+    m.host_status = d_status;
+    m.host_abort = d_hab;
+    m.tasks = (const amk_task_t*)(base + r_tasks.off);
+    m.queue_start = (const int32_t*)(base + r_queue.off);
+    m.lds_act = (int32_t)act;
+    m.part_stride = s.max_jobs;
+    m.lds_scr = (int32_t)scr;
+    m.lds_bytes = (int32_t)lds_bytes;
+
+    const int timeout_us = tuning && tuning->timeout_us > 0 ? tuning->timeout_us : 2000000;
+    h->timeout_ticks = (uint64_t)timeout_us * 100ull;  // the device wall clock runs at 100 MHz
+    *out = h;
+    return AMK_OK;
+  } catch (const std::bad_alloc&) {
+    free_handle(h);
+    return AMK_ERR_OUT_OF_MEMORY;
+  } catch (...) {
+    free_handle(h);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+}
+
+int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, float* logits, void* stream) {
+  if (!h || !kv_cache || !logits) return AMK_ERR_INVALID_ARGUMENT;
+  if (token < 0 || token >= h->s.V || pos < 0 || pos >= h->s.max_seq) return AMK_ERR_INVALID_ARGUMENT;
+  if (!aligned16(kv_cache) || !aligned16(logits)) return AMK_ERR_INVALID_ARGUMENT;
+  const int sticky = *(volatile int32_t*)h->h_status;
+  if (sticky != 0) return sticky;
+  DeviceGuard guard(h->device);
+  if (!guard.ok) return AMK_ERR_DEVICE;
+  const uint32_t epoch = h->epoch + 1;  // counter targets are epoch * producers, mod 2^32
+  const int st = amk_internal_launch(&h->dm, token, pos, epoch, (uint16_t*)kv_cache, logits, h->timeout_ticks,
+                                     stream);
+  if (st != AMK_OK) return st;
+  h->epoch = epoch;
+  h->last_stream = stream;
+  h->launched = true;
+  return AMK_OK;
+}
+
+const int32_t* amk_next_token_ptr(amk_handle_t h) { return h ? h->dm.next_token : nullptr; }
+
+int amk_copy_next_token(amk_handle_t h, int32_t* dst, void* stream) {
+  if (!h || !dst) return AMK_ERR_INVALID_ARGUMENT;
+  DeviceGuard guard(h->device);
+  if (hipMemcpyAsync(dst, h->dm.next_token, sizeof(int32_t), hipMemcpyDeviceToHost, (hipStream_t)stream) !=
+          hipSuccess ||
+      hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+    return AMK_ERR_DEVICE;
+  return AMK_OK;
+}
+
+int amk_get_status(amk_handle_t h) {
+  if (!h) return AMK_ERR_INVALID_ARGUMENT;
+  DeviceGuard guard(h->device);
+  if (h->launched && hipStreamSynchronize((hipStream_t)h->last_stream) != hipSuccess) return AMK_ERR_DEVICE;
+  return *(volatile int32_t*)h->h_status;
+}
+
+int amk_reset(amk_handle_t h) {
+  if (!h) return AMK_ERR_INVALID_ARGUMENT;
+  DeviceGuard guard(h->device);
+  if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
+  const size_t ctr_bytes = sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch.n_counters;
+  if (hipMemset(h->dm.counters, 0, ctr_bytes) != hipSuccess) return AMK_ERR_DEVICE;
+  if (hipMemset(h->dm.dev_abort, 0, sizeof(int32_t)) != hipSuccess) return AMK_ERR_DEVICE;
+  if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
+  *(volatile int32_t*)h->h_status = 0;
+  h->epoch = 0;
+  return AMK_OK;
+}
+
+int amk_set_abort(amk_handle_t h, int32_t value) {
+  if (!h) return AMK_ERR_INVALID_ARGUMENT;
+  __atomic_store_n(h->h_abort, value ? 1 : 0, __ATOMIC_SEQ_CST);
+  return AMK_OK;
+}
+
+int amk_destroy(amk_handle_t h) {
+  free_handle(h);
+  return AMK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// Device-side view of one handle: shape, borrowed weight pointers, handle-owned
+// scratch and the uploaded schedule.  Passed BY VALUE as the megakernel's
+// argument, so every field is a wave-uniform kernel-argument load.
+#pragma once
+
+#include <cstdint>
+
+#include "../../include/amk.h"
+
+namespace amk {
+
+enum { W_Q = 0, W_K, W_V, W_O, W_G, W_U, W_D, W_COUNT };
+
+struct DevLayer {
+  const void* w[W_COUNT];      // bf16 or int8 [out, in]
+  const float* s[W_COUNT];     // fp32 [out] for int8, else null
+  const uint16_t* attn_norm;   // bf16 [H]
+  const uint16_t* mlp_norm;    // bf16 [H]
+};
+
+// Counters live on separate 128-byte lines.
+constexpr int kCounterStride = 32;  // uint32 elements
+
+// Layout of one attention partial record for a (layer, kv head, split):
+// for each of the `group` query heads: [m, l, pad, pad, acc[head_dim]].
+constexpr int kPartHead = 4;  // floats before acc
+
+struct DevModel {
+  // shape
+  int32_t H, L, nq, nkv, hd, I, V, max_seq;
+  int32_t fmt;        // AMK_WEIGHTS_*
+  int32_t lm_int8;    // LM head stored as int8 + scales (untied W8A16)
+  int32_t group, half, half_log2, units, q_units, nsplit, n_lm;
+  int32_t n_cu;
+  float eps;
+  float attn_scale;   // 1 / sqrt(head_dim)
+  // weights (borrowed)
+  const uint16_t* embed;
+  const uint16_t* final_norm;
+  const void* lm_w;
+  const float* lm_s;
+  const DevLayer* layers;    // device array [L]
+  // handle-owned tables and scratch
+  const float2* rope;        // [max_seq][half] (cos, sin), computed in fp64 on the host
+  float* x;                  // residual stream [2L + 1][H]; slot 0 unused (embedding row is read directly)
+  float* q;                  // [L][nq * hd] roped queries
+  float* part;               // [L][nkv][nsplit][group][kPartHead + hd]
+  float* o;                  // [L][nq * hd] attention output
+  float* a;                  // [L][I] SwiGLU output
+  float* argp;               // [n_lm][2] (max logit, index as float bits)
+  int32_t* next_token;       // [1]
+  uint32_t* counters;        // [n_counters * kCounterStride]
+  int32_t* dev_abort;        // device word: nonzero stops every workgroup at its next wait
+  int32_t* host_status;      // host-mapped: first device error code
+  const int32_t* host_abort; // host-mapped: raised by amk_set_abort
+  const amk_task_t* tasks;   // sorted by (cu, seq)
+  const int32_t* queue_start;// [n_cu + 1]
+  // LDS layout (floats)
+  int32_t lds_act;           // activation vector region (padded to 1024, zero-filled tail)
+  int32_t part_stride;       // GEMV partials per streaming wave (max rows per task)
+  int32_t lds_scr;           // floats after the activation: GEMV partials or attention scratch
+  int32_t lds_bytes;         // dynamic LDS bytes of one workgroup
+};
+
+// Launch the decode-step megakernel (defined in megakernel.hip).
+extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos, uint32_t epoch,
+                                   uint16_t* kv, float* logits, uint64_t timeout_ticks, void* stream);
+// Threads per workgroup and LDS the kernel needs beyond the model-dependent regions.
+extern "C" int amk_internal_threads(void);
+extern "C" int amk_internal_attn_scratch(int group, int head_dim);
+extern "C" int amk_internal_prepare(int group, int lds_bytes);
+extern "C" int amk_internal_occupancy(int group, int lds_bytes, int* blocks_per_cu);
+
+}  // namespace amk

@@ -1,0 +1,521 @@
+// Lowering of one batch-1 decode step into per-CU task queues and the static
+// schedule check (paper §4 "The invariants validate() proves", Table
+// tab:checks; paper §3 Algorithm alg:sm for the queue walk it protects).
+#include "schedule.h"
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+
+namespace amk {
+
+namespace {
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+void set_msg(std::string* why, const char* fmt, long a = 0, long b = 0) {
+  if (!why) return;
+  char buf[256];
+  std::snprintf(buf, sizeof(buf), fmt, a, b);
+  *why = buf;
+}
+
+}  // namespace
+
+int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, Shape* s,
+                 std::string* why) {
+  if (!cfg || !s) { set_msg(why, "null config"); return AMK_ERR_INVALID_ARGUMENT; }
+  if (cfg->abi_version != AMK_ABI_VERSION) {
+    set_msg(why, "abi_version %ld, library speaks %ld", cfg->abi_version, AMK_ABI_VERSION);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  if (n_cu < 1) { set_msg(why, "n_cu %ld < 1", n_cu); return AMK_ERR_INVALID_ARGUMENT; }
+  const int H = cfg->hidden, L = cfg->n_layers, nq = cfg->n_heads, nkv = cfg->n_kv_heads;
+  const int hd = cfg->head_dim, I = cfg->intermediate, V = cfg->vocab, S = cfg->max_seq;
+  if (H <= 0 || L <= 0 || nq <= 0 || nkv <= 0 || hd <= 0 || I <= 0 || V <= 0 || S <= 0) {
+    set_msg(why, "all dimensions must be positive");
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  if (L > 65535) { set_msg(why, "n_layers %ld > 65535", L); return AMK_ERR_UNSUPPORTED; }
+  if (cfg->weight_format != AMK_WEIGHTS_BF16 && cfg->weight_format != AMK_WEIGHTS_W8A16) {
+    set_msg(why, "unknown weight_format %ld", cfg->weight_format);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  if (cfg->tied_embeddings != 0 && cfg->tied_embeddings != 1) {
+    set_msg(why, "tied_embeddings must be 0 or 1");
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  if (!(cfg->rope_theta > 0.f) || !(cfg->rms_eps >= 0.f)) {
+    set_msg(why, "rope_theta must be > 0 and rms_eps >= 0");
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  if (nq % nkv) { set_msg(why, "n_heads %ld not a multiple of n_kv_heads %ld", nq, nkv); return AMK_ERR_UNSUPPORTED; }
+  if (nq / nkv > 8) { set_msg(why, "query group %ld > 8", nq / nkv); return AMK_ERR_UNSUPPORTED; }
+  if (!is_pow2(hd) || hd < 64 || hd > 256) {
+    set_msg(why, "head_dim %ld must be a power of two in [64, 256]", hd);
+    return AMK_ERR_UNSUPPORTED;
+  }
+  // every weight row must be a whole number of 16-byte vectors in both formats
+  if (H % 16 || I % 16 || (nq * hd) % 16) {
+    set_msg(why, "hidden, intermediate and n_heads*head_dim must be multiples of 16");
+    return AMK_ERR_UNSUPPORTED;
+  }
+  int nsplit = tuning && tuning->attn_splits ? tuning->attn_splits : n_cu / nkv;
+  nsplit = std::max(1, std::min(nsplit, kMaxAttnSplits));
+  if (tuning && tuning->attn_splits && (tuning->attn_splits < 1 || tuning->attn_splits > kMaxAttnSplits)) {
+    set_msg(why, "attn_splits %ld outside [1, %ld]", tuning->attn_splits, kMaxAttnSplits);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  int max_jobs = tuning && tuning->max_rows_per_task ? tuning->max_rows_per_task : kMaxJobsPerTask;
+  if (max_jobs < 2 || max_jobs > kMaxJobsPerTask) {
+    set_msg(why, "max_rows_per_task %ld outside [2, %ld]", max_jobs, kMaxJobsPerTask);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  s->H = H; s->L = L; s->nq = nq; s->nkv = nkv; s->hd = hd; s->I = I; s->V = V; s->max_seq = S;
+  s->fmt = cfg->weight_format; s->tied = cfg->tied_embeddings;
+  s->group = nq / nkv; s->half = hd / 2;
+  s->units = (nq + 2 * nkv) * s->half; s->q_units = nq * s->half;
+  s->nsplit = nsplit; s->max_jobs = max_jobs;
+  s->theta = cfg->rope_theta; s->eps = cfg->rms_eps;
+  return AMK_OK;
+}
+
+int task_jobs(const Shape& s, const amk_task_t& t) {
+  const int n = t.end - t.begin;
+  switch (t.op) {
+    case AMK_OP_QKV: return 2 * n;
+    case AMK_OP_GATEUP: return 2 * n;
+    case AMK_OP_O: case AMK_OP_DOWN: case AMK_OP_LMHEAD: return n;
+    default: return 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// lowering
+// ---------------------------------------------------------------------------
+Schedule build_schedule(const Shape& s, int n_cu) {
+  Schedule sch;
+  std::vector<int> qlen(n_cu, 0);
+  int n_ctr = 0;
+  int rot = 0;  // rotating start CU for stages narrower than the grid
+
+  auto add = [&](int op, int layer, int cu, int b, int e, int aux,
+                 std::vector<std::pair<int, int>> waits, int sig) {
+    amk_task_t t;
+    std::memset(&t, 0, sizeof(t));
+    t.op = (uint16_t)op; t.layer = (uint16_t)layer; t.cu = cu; t.seq = qlen[cu]++;
+    t.begin = b; t.end = e; t.aux = aux;
+    t.n_wait = (int)waits.size();
+    for (int i = 0; i < AMK_MAX_WAITS; ++i) { t.wait_counter[i] = -1; t.wait_count[i] = 0; }
+    for (size_t i = 0; i < waits.size(); ++i) {
+      t.wait_counter[i] = waits[i].first; t.wait_count[i] = waits[i].second;
+    }
+    t.signal_counter = sig;
+    sch.tasks.push_back(t);
+  };
+  // number of tasks for a stage of `items` work items of `jobs_per_item` rows
+  auto n_tasks = [&](int items, int jobs_per_item) {
+    int n = std::min(n_cu, items);
+    int need = (int)(((long)items * jobs_per_item + s.max_jobs - 1) / s.max_jobs);
+    // each task must also hold whole items: ceil(items / n) * jobs_per_item <= max_jobs
+    n = std::max(n, need);
+    while (((items + n - 1) / n) * jobs_per_item > s.max_jobs) ++n;
+    return std::min(n, items);
+  };
+  auto cu_of = [&](int i, int n) { return n >= n_cu ? i % n_cu : (rot + i) % n_cu; };
+  auto bump = [&](int n) { if (n < n_cu) rot = (rot + n) % n_cu; };
+  auto lo = [](int total, int parts, int i) { return (int)((long)total * i / parts); };
+  // a stage of n tasks over `items` items, all waiting on (wc, wn), signalling sig
+  auto stage = [&](int op, int layer, int items, int jobs_per_item, int wc, int wn) {
+    const int n = n_tasks(items, jobs_per_item);
+    const int sig = n_ctr++;
+    for (int i = 0; i < n; ++i) {
+      std::vector<std::pair<int, int>> w;
+      if (wc >= 0) w.push_back({wc, wn});
+      add(op, layer, cu_of(i, n), lo(items, n, i), lo(items, n, i + 1), 0, w, sig);
+    }
+    bump(n);
+    return std::make_pair(sig, n);
+  };
+
+  int prev_c = -1, prev_n = 0;  // counter of the stage producing the layer input
+  for (int l = 0; l < s.L; ++l) {
+    auto qkv = stage(AMK_OP_QKV, l, s.units, 2, prev_c, prev_n);
+    // attention: one task per (KV head, position split)
+    const int c_attn = n_ctr++;
+    const int n_attn = s.nkv * s.nsplit;
+    for (int i = 0; i < n_attn; ++i) {
+      add(AMK_OP_ATTN, l, cu_of(i, n_attn), i % s.nsplit, s.nsplit, i / s.nsplit,
+          {{qkv.first, qkv.second}}, c_attn);
+    }
+    bump(n_attn);
+    auto comb = stage(AMK_OP_COMBINE, l, s.nq, 0, c_attn, n_attn);
+    auto o = stage(AMK_OP_O, l, s.H, 1, comb.first, comb.second);
+    auto gu = stage(AMK_OP_GATEUP, l, s.I, 2, o.first, o.second);
+    auto dn = stage(AMK_OP_DOWN, l, s.H, 1, gu.first, gu.second);
+    prev_c = dn.first; prev_n = dn.second;
+  }
+  // LM head: one argmax partial slot per task
+  {
+    const int n = n_tasks(s.V, 1);
+    const int sig = n_ctr++;
+    for (int i = 0; i < n; ++i)
+      add(AMK_OP_LMHEAD, 0, cu_of(i, n), lo(s.V, n, i), lo(s.V, n, i + 1), i, {{prev_c, prev_n}}, sig);
+    bump(n);
+    add(AMK_OP_ARGMAX, 0, cu_of(0, 1), 0, n, 0, {{sig, n}}, -1);
+    sch.n_lm_slots = n;
+  }
+  sch.n_counters = n_ctr;
+  finalize_queues(&sch.tasks, n_cu, &sch.queue_start);
+  return sch;
+}
+
+void finalize_queues(std::vector<amk_task_t>* tasks, int n_cu, std::vector<int32_t>* queue_start) {
+  std::stable_sort(tasks->begin(), tasks->end(), [](const amk_task_t& a, const amk_task_t& b) {
+    return a.cu != b.cu ? a.cu < b.cu : a.seq < b.seq;
+  });
+  queue_start->assign(n_cu + 1, 0);
+  for (const auto& t : *tasks) (*queue_start)[t.cu + 1]++;
+  for (int c = 0; c < n_cu; ++c) (*queue_start)[c + 1] += (*queue_start)[c];
+}
+
+// ---------------------------------------------------------------------------
+// static check
+// ---------------------------------------------------------------------------
+namespace {
+
+// Buffers a task reads or writes within one launch.  Index spaces:
+//   X(i)   i in [0, 2L]: residual stream, H elements; X(0) is the gathered
+//          embedding row (an input, written by nobody)
+//   Q(l)   q/RoPE units: n_heads * d/2
+//   KV(l)  appended K and V row-pair units: 2 * n_kv * d/2 (K first)
+//   PART(l) attention partial slots: n_kv * nsplit
+//   O(l)   attention output: n_heads * d
+//   A(l)   SwiGLU output: I
+//   LOGITS V;  ARGP n_lm_slots;  NEXT 1
+enum BufKind { B_X = 0, B_Q, B_KV, B_PART, B_O, B_A, B_LOGITS, B_ARGP, B_NEXT };
+
+struct Access {
+  int buf;  // dense buffer id
+  int lo, hi;
+};
+
+struct BufIds {
+  int L;
+  int x(int i) const { return i; }
+  int q(int l) const { return 2 * L + 1 + l; }
+  int kv(int l) const { return 3 * L + 1 + l; }
+  int part(int l) const { return 4 * L + 1 + l; }
+  int o(int l) const { return 5 * L + 1 + l; }
+  int a(int l) const { return 6 * L + 1 + l; }
+  int logits() const { return 7 * L + 1; }
+  int argp() const { return 7 * L + 2; }
+  int next() const { return 7 * L + 3; }
+  int count() const { return 7 * L + 4; }
+  bool is_kv(int b) const { return b >= 3 * L + 1 && b < 4 * L + 1; }
+};
+
+void accesses(const Shape& s, const BufIds& ids, const amk_task_t& t, std::vector<Access>* rd,
+              std::vector<Access>* wr) {
+  rd->clear(); wr->clear();
+  const int l = t.layer;
+  switch (t.op) {
+    case AMK_OP_QKV: {
+      rd->push_back({ids.x(2 * l), 0, s.H});
+      const int qb = std::min(t.end, s.q_units);
+      if (t.begin < qb) wr->push_back({ids.q(l), t.begin, qb});
+      const int kb = std::max(t.begin, s.q_units);
+      if (kb < t.end) wr->push_back({ids.kv(l), kb - s.q_units, t.end - s.q_units});
+      break;
+    }
+    case AMK_OP_ATTN: {
+      const int g = t.aux;
+      rd->push_back({ids.kv(l), g * s.half, (g + 1) * s.half});                         // K head g
+      rd->push_back({ids.kv(l), (s.nkv + g) * s.half, (s.nkv + g + 1) * s.half});       // V head g
+      rd->push_back({ids.q(l), g * s.group * s.half, (g + 1) * s.group * s.half});
+      wr->push_back({ids.part(l), g * s.nsplit + t.begin, g * s.nsplit + t.begin + 1});
+      break;
+    }
+    case AMK_OP_COMBINE: {
+      const int g0 = t.begin / s.group, g1 = (t.end - 1) / s.group + 1;
+      rd->push_back({ids.part(l), g0 * s.nsplit, g1 * s.nsplit});
+      wr->push_back({ids.o(l), t.begin * s.hd, t.end * s.hd});
+      break;
+    }
+    case AMK_OP_O:
+      rd->push_back({ids.o(l), 0, s.nq * s.hd});
+      rd->push_back({ids.x(2 * l), t.begin, t.end});
+      wr->push_back({ids.x(2 * l + 1), t.begin, t.end});
+      break;
+    case AMK_OP_GATEUP:
+      rd->push_back({ids.x(2 * l + 1), 0, s.H});
+      wr->push_back({ids.a(l), t.begin, t.end});
+      break;
+    case AMK_OP_DOWN:
+      rd->push_back({ids.a(l), 0, s.I});
+      rd->push_back({ids.x(2 * l + 1), t.begin, t.end});
+      wr->push_back({ids.x(2 * l + 2), t.begin, t.end});
+      break;
+    case AMK_OP_LMHEAD:
+      rd->push_back({ids.x(2 * s.L), 0, s.H});
+      wr->push_back({ids.logits(), t.begin, t.end});
+      wr->push_back({ids.argp(), t.aux, t.aux + 1});
+      break;
+    case AMK_OP_ARGMAX:
+      rd->push_back({ids.argp(), t.begin, t.end});
+      wr->push_back({ids.next(), 0, 1});
+      break;
+    default: break;
+  }
+}
+
+struct Reporter {
+  amk_check_report_t* r;
+  bool fail(int rule, int task, int other, const char* fmt, long a = 0, long b = 0, long c = 0) {
+    r->ok = 0; r->rule = rule; r->task = task; r->other = other;
+    std::snprintf(r->message, sizeof(r->message), fmt, a, b, c);
+    return false;
+  }
+};
+
+}  // namespace
+
+bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, int n_counters,
+                    amk_check_report_t* rep) {
+  std::memset(rep, 0, sizeof(*rep));
+  rep->ok = 1; rep->rule = AMK_CHECK_OK; rep->task = -1; rep->other = -1;
+  rep->n_tasks = n; rep->n_counters = n_counters;
+  Reporter R{rep};
+  if (n <= 0 || !tasks) return R.fail(AMK_CHECK_WELL_FORMED, -1, -1, "empty schedule");
+  if (n_counters < 0) return R.fail(AMK_CHECK_WELL_FORMED, -1, -1, "negative counter count");
+
+  // ---- 1. well-formedness and capacity -----------------------------------
+  int n_lm = 0;
+  for (int i = 0; i < n; ++i)
+    if (tasks[i].op == AMK_OP_LMHEAD) ++n_lm;
+  std::vector<int> qlen(n_cu, 0);
+  for (int i = 0; i < n; ++i) {
+    const amk_task_t& t = tasks[i];
+    if (t.op < AMK_OP_QKV || t.op > AMK_OP_ARGMAX)
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: unknown op %ld", i, t.op);
+    if (t.cu < 0 || t.cu >= n_cu)
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: queue %ld out of range", i, t.cu);
+    const bool layered = t.op <= AMK_OP_DOWN;
+    if (layered && t.layer >= s.L)
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: layer %ld out of range", i, t.layer);
+    if (t.n_wait < 0 || t.n_wait > AMK_MAX_WAITS)
+      return R.fail(AMK_CHECK_CAPACITY, i, -1, "task %ld: %ld waits (cap 4)", i, t.n_wait);
+    for (int w = 0; w < t.n_wait; ++w)
+      if (t.wait_counter[w] < 0 || t.wait_counter[w] >= n_counters)
+        return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: wait on counter %ld out of range", i,
+                      t.wait_counter[w]);
+    if (t.signal_counter < -1 || t.signal_counter >= n_counters)
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: signal counter %ld out of range", i,
+                    t.signal_counter);
+    int lim = 0;
+    switch (t.op) {
+      case AMK_OP_QKV: lim = s.units; break;
+      case AMK_OP_ATTN: lim = s.nsplit; break;
+      case AMK_OP_COMBINE: lim = s.nq; break;
+      case AMK_OP_O: case AMK_OP_DOWN: lim = s.H; break;
+      case AMK_OP_GATEUP: lim = s.I; break;
+      case AMK_OP_LMHEAD: lim = s.V; break;
+      case AMK_OP_ARGMAX: lim = n_lm; break;
+    }
+    if (t.op == AMK_OP_ATTN) {
+      if (t.end != s.nsplit || t.begin < 0 || t.begin >= s.nsplit || t.aux < 0 || t.aux >= s.nkv)
+        return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: bad attention split/head", i);
+    } else if (t.begin < 0 || t.end > lim || t.begin >= t.end) {
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: range [%ld, ...) out of bounds", i, t.begin);
+    }
+    if (t.op == AMK_OP_ARGMAX && (t.begin != 0 || t.end != n_lm))
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: argmax must reduce all %ld partial slots", i, n_lm);
+    if (t.op == AMK_OP_LMHEAD && (t.aux < 0 || t.aux >= n_lm))
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: argmax slot %ld out of range", i, t.aux);
+    if (task_jobs(s, t) > s.max_jobs)
+      return R.fail(AMK_CHECK_CAPACITY, i, -1, "task %ld: %ld rows exceed the per-task cap", i, task_jobs(s, t));
+    if (t.op == AMK_OP_COMBINE && t.end - t.begin > 64)
+      return R.fail(AMK_CHECK_CAPACITY, i, -1, "task %ld: combine of more than 64 heads", i);
+    qlen[t.cu]++;
+  }
+  // queue positions must be 0..len-1, each exactly once
+  {
+    std::vector<std::vector<int>> at(n_cu);
+    for (int c = 0; c < n_cu; ++c) at[c].assign(qlen[c], -1);
+    for (int i = 0; i < n; ++i) {
+      const amk_task_t& t = tasks[i];
+      if (t.seq < 0 || t.seq >= qlen[t.cu] || at[t.cu][t.seq] != -1)
+        return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: queue position %ld invalid or repeated", i, t.seq);
+      at[t.cu][t.seq] = i;
+    }
+  }
+
+  // ---- 2. wait satisfiability and all-join ----------------------------------
+  std::vector<std::vector<int>> producers(n_counters), waiters(n_counters);
+  for (int i = 0; i < n; ++i) {
+    if (tasks[i].signal_counter >= 0) producers[tasks[i].signal_counter].push_back(i);
+    for (int w = 0; w < tasks[i].n_wait; ++w) waiters[tasks[i].wait_counter[w]].push_back(i);
+  }
+  for (int i = 0; i < n; ++i) {
+    const amk_task_t& t = tasks[i];
+    for (int w = 0; w < t.n_wait; ++w) {
+      const int c = t.wait_counter[w], need = t.wait_count[w];
+      const int np = (int)producers[c].size();
+      if (need < 1) return R.fail(AMK_CHECK_WAIT_SATISFIABLE, i, c, "task %ld waits for %ld < 1 signals", i, need);
+      if (np == 0) return R.fail(AMK_CHECK_WAIT_SATISFIABLE, i, c, "task %ld waits on counter %ld that nobody signals", i, c);
+      if (need > np)
+        return R.fail(AMK_CHECK_WAIT_SATISFIABLE, i, c, "task %ld needs %ld signals, counter has %ld producers", i, need, np);
+      if (need != np)
+        return R.fail(AMK_CHECK_ALL_JOIN, i, c, "task %ld waits for %ld of %ld producers (which-producer race)", i, need, np);
+    }
+  }
+
+  // ---- 3. queue order: a producer on the same CU must be queued earlier ------
+  long n_edges = 0;
+  for (int i = 0; i < n; ++i) {
+    const amk_task_t& t = tasks[i];
+    for (int w = 0; w < t.n_wait; ++w) {
+      for (int p : producers[t.wait_counter[w]]) {
+        ++n_edges;
+        if (tasks[p].cu == t.cu && tasks[p].seq >= t.seq)
+          return R.fail(AMK_CHECK_QUEUE_ORDER, i, p, "task %ld on queue %ld waits on task %ld queued at or after it", i,
+                        t.cu, p);
+      }
+    }
+  }
+  rep->n_edges = (int)std::min<long>(n_edges, 0x7fffffff);
+
+  // ---- 4. acyclicity of (counter edges + queue-order edges): Kahn ------------
+  // A task is ready when its queue predecessor has run and every counter it
+  // waits on has all its producers run.  The order found is also a valid
+  // global order for the happens-before pass below.
+  std::vector<std::vector<int>> queue(n_cu);
+  for (int c = 0; c < n_cu; ++c) queue[c].assign(qlen[c], -1);
+  for (int i = 0; i < n; ++i) queue[tasks[i].cu][tasks[i].seq] = i;
+  std::vector<int> indeg(n, 0), remaining(n_counters);
+  for (int c = 0; c < n_counters; ++c) remaining[c] = (int)producers[c].size();
+  for (int i = 0; i < n; ++i) indeg[i] = (tasks[i].seq > 0 ? 1 : 0) + tasks[i].n_wait;
+  std::vector<int> order;
+  order.reserve(n);
+  std::vector<int> stack;
+  for (int i = 0; i < n; ++i)
+    if (indeg[i] == 0) stack.push_back(i);
+  while (!stack.empty()) {
+    const int i = stack.back();
+    stack.pop_back();
+    order.push_back(i);
+    const amk_task_t& t = tasks[i];
+    if (t.seq + 1 < qlen[t.cu]) {
+      const int nx = queue[t.cu][t.seq + 1];
+      if (--indeg[nx] == 0) stack.push_back(nx);
+    }
+    if (t.signal_counter >= 0 && --remaining[t.signal_counter] == 0) {
+      for (int wt : waiters[t.signal_counter])
+        if (--indeg[wt] == 0) stack.push_back(wt);
+    }
+  }
+  if ((int)order.size() != n) {
+    // witness: walk "blocked by" edges from an unscheduled task until a repeat
+    std::vector<char> done(n, 0);
+    for (int i : order) done[i] = 1;
+    int cur = -1;
+    for (int i = 0; i < n; ++i)
+      if (!done[i]) { cur = i; break; }
+    std::vector<int> seen(n, -1);
+    int step = 0;
+    while (cur >= 0 && seen[cur] < 0) {
+      seen[cur] = step++;
+      const amk_task_t& t = tasks[cur];
+      int nxt = -1;
+      if (t.seq > 0 && !done[queue[t.cu][t.seq - 1]]) nxt = queue[t.cu][t.seq - 1];
+      for (int w = 0; nxt < 0 && w < t.n_wait; ++w)
+        for (int p : producers[t.wait_counter[w]])
+          if (!done[p]) { nxt = p; break; }
+      cur = nxt;
+    }
+    return R.fail(AMK_CHECK_ACYCLIC, cur, -1,
+                  "deadlock: %ld tasks can never run; cycle through task %ld (cycle length %ld)",
+                  n - (long)order.size(), cur, cur >= 0 ? step - seen[cur] : 0);
+  }
+
+  // ---- 5. happens-before (vector clocks over queues): every read of a region
+  //         written in this launch must be ordered after all its writers -------
+  BufIds ids{s.L};
+  const int nb = ids.count();
+  std::vector<int> buf_size(nb, 0);
+  for (int i = 0; i <= 2 * s.L; ++i) buf_size[ids.x(i)] = s.H;
+  for (int l = 0; l < s.L; ++l) {
+    buf_size[ids.q(l)] = s.q_units;
+    buf_size[ids.kv(l)] = 2 * s.nkv * s.half;
+    buf_size[ids.part(l)] = s.nkv * s.nsplit;
+    buf_size[ids.o(l)] = s.nq * s.hd;
+    buf_size[ids.a(l)] = s.I;
+  }
+  buf_size[ids.logits()] = s.V;
+  buf_size[ids.argp()] = n_lm;
+  buf_size[ids.next()] = 1;
+
+  struct W { int lo, hi, task; };
+  std::vector<std::vector<W>> writers(nb);
+  std::vector<Access> rd, wr;
+  for (int i = 0; i < n; ++i) {
+    accesses(s, ids, tasks[i], &rd, &wr);
+    for (auto& a : wr) writers[a.buf].push_back({a.lo, a.hi, i});
+  }
+  // exactly-once outputs: writer intervals of each written buffer tile it
+  for (int b = 0; b < nb; ++b) {
+    auto& v = writers[b];
+    if (b == ids.x(0)) {
+      if (!v.empty()) return R.fail(AMK_CHECK_OUTPUT, v[0].task, -1, "task %ld writes the embedding input", v[0].task);
+      continue;
+    }
+    std::sort(v.begin(), v.end(), [](const W& a, const W& c) { return a.lo < c.lo; });
+    int at = 0;
+    for (auto& w : v) {
+      if (w.lo < at) return R.fail(AMK_CHECK_OUTPUT, w.task, -1, "task %ld rewrites a region of buffer %ld", w.task, b);
+      if (w.lo > at) return R.fail(AMK_CHECK_OUTPUT, w.task, -1, "buffer %ld region [%ld, ...) is never written", b, at);
+      at = w.hi;
+    }
+    if (at != buf_size[b])
+      return R.fail(AMK_CHECK_OUTPUT, -1, -1, "buffer %ld written up to %ld only", b, at);
+  }
+
+  // vector clocks: vc[c] = highest queue position on CU c that happened before
+  std::vector<int32_t> q_vc((size_t)n_cu * n_cu, -1);        // clock of each queue's last task
+  std::vector<int32_t> ctr_vc((size_t)n_counters * n_cu, -1);// join of each counter's producers
+  std::vector<int> ctr_left(n_counters);
+  for (int c = 0; c < n_counters; ++c) ctr_left[c] = (int)producers[c].size();
+  std::vector<int32_t> vc(n_cu);
+  for (int i : order) {
+    const amk_task_t& t = tasks[i];
+    std::copy(q_vc.begin() + (size_t)t.cu * n_cu, q_vc.begin() + (size_t)(t.cu + 1) * n_cu, vc.begin());
+    for (int w = 0; w < t.n_wait; ++w) {
+      const int32_t* cv = &ctr_vc[(size_t)t.wait_counter[w] * n_cu];
+      for (int c = 0; c < n_cu; ++c) vc[c] = std::max(vc[c], cv[c]);
+    }
+    vc[t.cu] = t.seq;
+    // reads
+    accesses(s, ids, t, &rd, &wr);
+    for (auto& a : rd) {
+      for (auto& w : writers[a.buf]) {
+        if (w.hi <= a.lo || w.lo >= a.hi) continue;
+        const amk_task_t& wt = tasks[w.task];
+        if (w.task == i) continue;
+        if (vc[wt.cu] < wt.seq) {
+          const int rule = ids.is_kv(a.buf) ? AMK_CHECK_KV_ORDER : AMK_CHECK_RACE;
+          return R.fail(rule, i, w.task, "task %ld reads buffer %ld before writer task %ld is ordered", i, a.buf,
+                        w.task);
+        }
+      }
+    }
+    std::copy(vc.begin(), vc.end(), q_vc.begin() + (size_t)t.cu * n_cu);
+    if (t.signal_counter >= 0) {
+      int32_t* cv = &ctr_vc[(size_t)t.signal_counter * n_cu];
+      for (int c = 0; c < n_cu; ++c) cv[c] = std::max(cv[c], vc[c]);
+    }
+  }
+  return true;
+}
+
+}  // namespace amk

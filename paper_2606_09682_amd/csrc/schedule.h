@@ -1,0 +1,58 @@
+// Host-side lowering of one decode step into per-CU task queues, and the
+// static check that must accept a schedule before it is launched.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/amk.h"
+
+namespace amk {
+
+// Largest number of GEMV output rows one task may own: the kernel keeps one
+// fp32 partial per row and streaming wave in LDS.
+constexpr int kMaxJobsPerTask = 1024;
+// Largest number of position splits per KV head (one combine lane per split).
+constexpr int kMaxAttnSplits = 64;
+
+// Derived shape of a validated config.
+struct Shape {
+  int H = 0, L = 0, nq = 0, nkv = 0, hd = 0, I = 0, V = 0, max_seq = 0;
+  int fmt = 0, tied = 0;
+  int group = 0;         // query heads per KV head
+  int half = 0;          // hd / 2: RoPE row pairs per head
+  int units = 0;         // (nq + 2 nkv) * half: q/k/v row-pair units
+  int q_units = 0;       // nq * half
+  int nsplit = 0;        // attention position splits per KV head
+  int max_jobs = 0;      // GEMV rows per task cap
+  float theta = 0.f, eps = 0.f;
+};
+
+// Validates the config (shape family, divisibility, 16-byte row alignment)
+// and fills *s.  Returns AMK_OK or AMK_ERR_INVALID_ARGUMENT / _UNSUPPORTED
+// with a message.
+int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, Shape* s,
+                 std::string* why);
+
+struct Schedule {
+  std::vector<amk_task_t> tasks;   // sorted by (cu, seq)
+  std::vector<int32_t> queue_start;// n_cu + 1 offsets into tasks
+  int n_counters = 0;
+  int n_lm_slots = 0;              // argmax partial slots (one per LM-head task)
+};
+
+// Deterministic lowering of one decode step onto n_cu queues.
+Schedule build_schedule(const Shape& s, int n_cu);
+
+// Static check (never throws).  Fills *rep; returns true iff accepted.
+bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n_tasks,
+                    int n_counters, amk_check_report_t* rep);
+
+// Sorts tasks by (cu, seq) and computes queue offsets (tasks must be checked).
+void finalize_queues(std::vector<amk_task_t>* tasks, int n_cu, std::vector<int32_t>* queue_start);
+
+// Number of rows (jobs) a GEMV task computes; 0 for non-GEMV ops.
+int task_jobs(const Shape& s, const amk_task_t& t);
+
+}  // namespace amk

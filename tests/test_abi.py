@@ -1,0 +1,155 @@
+"""The C ABI library loads, exports every function include/amk.h declares, and
+its ctypes mirror agrees with the header's layouts and constants (no GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import synth
+from paper_2606_09682_amd import amk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "amk.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(amk.LIB_PATH):
+        from paper_2606_09682_amd import build
+        build.build()
+    return amk.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(amk_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", amk.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (amk_\w+)", out))
+    assert set(names) <= exported
+
+
+def _c_layout():
+    """Compile a C program against amk.h that prints sizes, offsets and enum values."""
+    src = r'''
+#include <stdio.h>
+#include <stddef.h>
+#include "amk.h"
+#define S(t) printf("sizeof %s %zu\n", #t, sizeof(t));
+#define O(t, f) printf("offsetof %s.%s %zu\n", #t, #f, offsetof(t, f));
+#define E(v) printf("enum %s %d\n", #v, (int)(v));
+int main(void) {
+  S(amk_config_t) S(amk_linear_t) S(amk_layer_weights_t) S(amk_weights_t) S(amk_tuning_t) S(amk_task_t)
+  S(amk_check_report_t)
+  O(amk_config_t, rope_theta) O(amk_config_t, device) O(amk_layer_weights_t, down) O(amk_weights_t, layers)
+  O(amk_task_t, wait_counter) O(amk_task_t, wait_count) O(amk_task_t, signal_counter) O(amk_check_report_t, message)
+  E(AMK_ABI_VERSION) E(AMK_OK) E(AMK_ERR_INVALID_ARGUMENT) E(AMK_ERR_UNSUPPORTED) E(AMK_ERR_SCHEDULE_REJECTED)
+  E(AMK_ERR_OUT_OF_MEMORY) E(AMK_ERR_DEVICE) E(AMK_ERR_COOPERATIVE_UNSUPPORTED) E(AMK_ERR_TIMEOUT)
+  E(AMK_ERR_BAD_STATE) E(AMK_ERR_ABORTED) E(AMK_WEIGHTS_BF16) E(AMK_WEIGHTS_W8A16) E(AMK_MAX_WAITS)
+  E(AMK_OP_QKV) E(AMK_OP_ATTN) E(AMK_OP_COMBINE) E(AMK_OP_O) E(AMK_OP_GATEUP) E(AMK_OP_DOWN) E(AMK_OP_LMHEAD)
+  E(AMK_OP_ARGMAX) E(AMK_CHECK_OK) E(AMK_CHECK_WELL_FORMED) E(AMK_CHECK_CAPACITY) E(AMK_CHECK_WAIT_SATISFIABLE)
+  E(AMK_CHECK_ALL_JOIN) E(AMK_CHECK_ACYCLIC) E(AMK_CHECK_QUEUE_ORDER) E(AMK_CHECK_RACE) E(AMK_CHECK_KV_ORDER)
+  E(AMK_CHECK_OUTPUT)
+  return 0;
+}
+'''
+    import tempfile
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "layout.c")
+        exe = os.path.join(d, "layout")
+        open(c, "w").write(src)
+        subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), c, "-o", exe],
+                       check=True)
+        out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout
+    res = {}
+    for line in out.splitlines():
+        kind, name, val = line.split()
+        res[(kind, name)] = int(val)
+    return res
+
+
+def test_ctypes_mirror_matches_header():
+    c = _c_layout()
+    for t in ("amk_config_t", "amk_linear_t", "amk_layer_weights_t", "amk_weights_t", "amk_tuning_t", "amk_task_t",
+              "amk_check_report_t"):
+        assert ctypes.sizeof(getattr(amk, t)) == c[("sizeof", t)], t
+    assert c[("sizeof", "amk_task_t")] == 64
+    for key, val in c.items():
+        kind, name = key
+        if kind == "offsetof":
+            t, f = name.split(".")
+            assert getattr(getattr(amk, t), f).offset == val, name
+        elif kind == "enum":
+            assert getattr(amk, name) == val, name
+
+
+def test_status_strings(lib):
+    for code in range(0, -10, -1):
+        assert amk.amk_status_string(code) not in ("", "unknown status")
+    assert amk.amk_status_string(-99) == "unknown status"
+
+
+def _cfg(name, fmt="bf16", **over):
+    c = synth.get(name)
+    kw = dict(hidden=c.hidden, n_layers=c.n_layers, n_heads=c.n_heads, n_kv_heads=c.n_kv_heads,
+              head_dim=c.head_dim, intermediate=c.intermediate, vocab=c.vocab, max_seq=c.seq_capacity,
+              rope_theta=c.rope_theta, rms_eps=c.rms_eps, tied_embeddings=c.tied_embeddings, weight_format=fmt)
+    kw.update(over)
+    return amk.make_config(**kw)
+
+
+@pytest.mark.parametrize("name", list(synth.CONFIGS))
+def test_kv_cache_bytes(lib, name):
+    c = synth.get(name)
+    want = c.n_layers * 2 * c.n_kv_heads * c.seq_capacity * c.head_dim * 2
+    assert amk.amk_kv_cache_bytes(_cfg(name)) == want
+
+
+@pytest.mark.parametrize("name", list(synth.CONFIGS))
+@pytest.mark.parametrize("n_cu", [256, 80, 7, 1])
+@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+def test_every_workload_schedule_is_accepted(lib, name, n_cu, fmt):
+    assert amk.amk_check_config(_cfg(name, fmt), n_cu) == amk.AMK_OK
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(n_kv_heads=3), amk.AMK_ERR_UNSUPPORTED),            # 4 heads not a multiple of 3 KV heads
+    (dict(head_dim=96), amk.AMK_ERR_UNSUPPORTED),             # not a power of two
+    (dict(head_dim=32), amk.AMK_ERR_UNSUPPORTED),             # below the attention tiling minimum
+    (dict(hidden=200), amk.AMK_ERR_UNSUPPORTED),              # rows not whole 16-byte vectors
+    (dict(intermediate=690), amk.AMK_ERR_UNSUPPORTED),
+    (dict(n_heads=32, n_kv_heads=2), amk.AMK_ERR_UNSUPPORTED),# group of 16 heads
+    (dict(vocab=0), amk.AMK_ERR_INVALID_ARGUMENT),
+    (dict(weight_format=7), amk.AMK_ERR_INVALID_ARGUMENT),
+])
+def test_unsupported_configs_are_rejected(lib, over, status):
+    cfg = _cfg("tiny")
+    for k, v in over.items():
+        setattr(cfg, k, v)
+    assert amk.amk_check_config(cfg, 256) == status
+
+
+def test_bad_abi_version_rejected(lib):
+    cfg = _cfg("tiny")
+    cfg.abi_version = 99
+    assert amk.amk_check_config(cfg, 256) == amk.AMK_ERR_INVALID_ARGUMENT
+
+
+def test_null_arguments_fail_cleanly(lib):
+    h = ctypes.c_void_p()
+    assert lib.amk_create(None, None, None, ctypes.byref(h)) == amk.AMK_ERR_INVALID_ARGUMENT
+    assert h.value is None
+    assert lib.amk_create(None, None, None, None) == amk.AMK_ERR_INVALID_ARGUMENT
+    assert lib.amk_decode_step(None, 0, 0, None, None, None) == amk.AMK_ERR_INVALID_ARGUMENT
+    assert lib.amk_get_status(None) == amk.AMK_ERR_INVALID_ARGUMENT
+    assert lib.amk_reset(None) == amk.AMK_ERR_INVALID_ARGUMENT
+    assert lib.amk_destroy(None) == amk.AMK_OK
+    assert amk.amk_kv_cache_bytes(amk.amk_config_t()) == 0

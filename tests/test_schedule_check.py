@@ -1,0 +1,247 @@
+"""The static schedule check (paper §4, Table tab:checks) on real lowerings and
+on single-injection mutants of the unsafe classes the paper's soundness study
+uses (Table tab:soundness), plus a cross-queue deadlock that per-queue order
+checks alone would miss.  CPU only."""
+import ctypes
+import random
+
+import pytest
+
+import synth
+from paper_2606_09682_amd import amk
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import os
+    if not os.path.exists(amk.LIB_PATH):
+        from paper_2606_09682_amd import build
+        build.build()
+    return amk.load()
+
+
+def cfg_of(name, fmt="bf16"):
+    c = synth.get(name)
+    return amk.make_config(c.hidden, c.n_layers, c.n_heads, c.n_kv_heads, c.head_dim, c.intermediate, c.vocab,
+                           c.seq_capacity, c.rope_theta, c.rms_eps, c.tied_embeddings, fmt)
+
+
+N_CU = 16
+
+
+@pytest.fixture(scope="module")
+def tiny_sched(lib):
+    cfg = cfg_of("tiny")
+    tasks, nc = amk.amk_schedule_export(cfg, N_CU)
+    return cfg, tasks, nc
+
+
+def clone(tasks):
+    arr = (amk.amk_task_t * len(tasks))()
+    ctypes.memmove(arr, tasks, ctypes.sizeof(arr))
+    return arr
+
+
+def check(cfg, tasks, nc, n_cu=N_CU):
+    return amk.amk_schedule_check(cfg, n_cu, tasks, nc)
+
+
+def find(tasks, op, layer=None, pred=None):
+    for i, t in enumerate(tasks):
+        if t.op == op and (layer is None or t.layer == layer) and (pred is None or pred(t)):
+            return i
+    raise LookupError
+
+
+def producers(tasks, c):
+    return [i for i, t in enumerate(tasks) if t.signal_counter == c]
+
+
+@pytest.mark.parametrize("name", list(synth.CONFIGS))
+@pytest.mark.parametrize("n_cu", [256, 13])
+def test_real_lowering_accepted(lib, name, n_cu):
+    cfg = cfg_of(name, "w8a16")
+    tasks, nc = amk.amk_schedule_export(cfg, n_cu)
+    rep = check(cfg, tasks, nc, n_cu)
+    assert rep.ok == 1, rep.message
+    # one queue per CU, every queue used, seq contiguous
+    seen = {}
+    for t in tasks:
+        seen.setdefault(t.cu, []).append(t.seq)
+    assert sorted(seen) == list(range(n_cu))
+    for c, seqs in seen.items():
+        assert sorted(seqs) == list(range(len(seqs)))
+
+
+def test_schedule_shape_8b(lib):
+    cfg = cfg_of("llama3_8b")
+    tasks, nc = amk.amk_schedule_export(cfg, 256)
+    ops = [t.op for t in tasks]
+    L = 32
+    assert ops.count(amk.AMK_OP_QKV) == 256 * L
+    assert ops.count(amk.AMK_OP_ATTN) == 8 * 32 * L
+    assert ops.count(amk.AMK_OP_O) == 256 * L
+    assert ops.count(amk.AMK_OP_GATEUP) == 256 * L
+    assert ops.count(amk.AMK_OP_DOWN) == 256 * L
+    assert ops.count(amk.AMK_OP_LMHEAD) == 256
+    assert ops.count(amk.AMK_OP_ARGMAX) == 1
+    # every QKV task owns whole RoPE row pairs: 48 heads * 64 pairs / 256 = 12 units each
+    assert {t.end - t.begin for t in tasks if t.op == amk.AMK_OP_QKV} == {12}
+
+
+# ------------------------------------------------------------------ mutants
+def test_cycle_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_QKV, 0)
+    j = find(m, amk.AMK_OP_DOWN, 1)
+    c = m[j].signal_counter
+    t = m[i]
+    t.wait_counter[t.n_wait] = c
+    t.wait_count[t.n_wait] = len(producers(m, c))
+    t.n_wait += 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule in (amk.AMK_CHECK_ACYCLIC, amk.AMK_CHECK_QUEUE_ORDER), rep.message
+
+
+def test_drop_wait_race_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_O, 1)
+    m[i].n_wait = 0
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_RACE, rep.message
+
+
+def test_kv_read_before_append_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_ATTN, 2)
+    m[i].n_wait = 0
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_KV_ORDER, rep.message
+
+
+def test_self_wait_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_GATEUP, 0)
+    t = m[i]
+    c = t.signal_counter
+    t.wait_counter[t.n_wait] = c
+    t.wait_count[t.n_wait] = len(producers(m, c))
+    t.n_wait += 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_QUEUE_ORDER, rep.message
+
+
+def test_oob_counter_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    m[find(m, amk.AMK_OP_DOWN, 0)].wait_counter[0] = nc
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_WELL_FORMED, rep.message
+
+
+def test_oob_buffer_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_O, 0, lambda t: t.end == 256)
+    m[i].end = 257
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_WELL_FORMED, rep.message
+
+
+def test_capacity_overflow_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    m[find(m, amk.AMK_OP_QKV, 1)].n_wait = 5
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_CAPACITY, rep.message
+
+
+def test_partial_shared_wait_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_GATEUP, 1)
+    assert m[i].wait_count[0] > 2
+    m[i].wait_count[0] -= 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_ALL_JOIN, rep.message
+
+
+def test_unsatisfiable_waits_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_DOWN, 0)
+    m[i].wait_count[0] += 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_WAIT_SATISFIABLE
+    m = clone(tasks)
+    m[i].wait_count[0] = 0
+    assert check(cfg, m, nc).rule == amk.AMK_CHECK_WAIT_SATISFIABLE
+    # a counter nobody signals: retarget its only producers' signals
+    m = clone(tasks)
+    c = m[i].wait_counter[0]
+    for p in producers(m, c):
+        m[p].signal_counter = -1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_WAIT_SATISFIABLE
+
+
+def test_cross_queue_deadlock_rejected(lib):
+    """A deadlock that no single queue shows: the argmax task (queue x) gets a
+    fresh signal counter, and an early task A on the other queue y waits on it.
+    Argmax waits on every LM-head task, including those queued on y after A.
+    Every wait is satisfiable, A's producer sits on another queue (so the
+    per-queue order rule passes), yet the queues block each other."""
+    cfg = cfg_of("tiny")
+    tasks, nc = amk.amk_schedule_export(cfg, 2)
+    m = clone(tasks)
+    g = find(m, amk.AMK_OP_ARGMAX)
+    x = m[g].cu
+    y = 1 - x
+    a = find(m, amk.AMK_OP_QKV, 0, lambda t: t.cu == y)
+    assert any(t.op == amk.AMK_OP_LMHEAD and t.cu == y and t.seq > m[a].seq for t in m)
+    m[g].signal_counter = nc
+    t = m[a]
+    t.wait_counter[t.n_wait] = nc
+    t.wait_count[t.n_wait] = 1
+    t.n_wait += 1
+    rep = check(cfg, m, nc + 1, 2)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_ACYCLIC, rep.message
+    assert "deadlock" in rep.message.decode()
+
+
+def test_duplicate_and_missing_output_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_DOWN, 2, lambda t: t.begin > 0)
+    m[i].begin -= 1  # overlaps its neighbour
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_OUTPUT, rep.message
+    m = clone(tasks)
+    m[i].begin += 1  # leaves a row unwritten
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_OUTPUT, rep.message
+
+
+def test_queue_position_duplicates_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    m[1].seq = m[0].seq
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_WELL_FORMED
+
+
+def test_random_single_mutations_never_crash(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    rng = random.Random(7)
+    fields = ["begin", "end", "aux", "n_wait", "signal_counter", "seq", "cu", "layer", "op"]
+    for _ in range(300):
+        m = clone(tasks)
+        i = rng.randrange(len(m))
+        f = rng.choice(fields)
+        setattr(m[i], f, getattr(m[i], f) + rng.choice([-3, -1, 1, 2, 1000]))
+        rep = check(cfg, m, nc)
+        assert rep.ok in (0, 1)
