@@ -64,7 +64,7 @@ typedef struct {
   int32_t n_layers;         /* L */
   int32_t n_heads;          /* query heads */
   int32_t n_kv_heads;       /* KV heads; n_heads % n_kv_heads == 0, n_heads / n_kv_heads <= 8 */
-  int32_t head_dim;         /* d; a power of two in [64, 256] */
+  int32_t head_dim;         /* d; 64 or 128 */
   int32_t intermediate;     /* SwiGLU width I */
   int32_t vocab;            /* V */
   int32_t max_seq;          /* KV cache capacity in positions */
@@ -107,6 +107,7 @@ typedef struct {
   int32_t attn_splits;      /* attention tasks per KV head (1..64); 0 = derived from the CU count */
   int32_t timeout_us;       /* deadline of one device counter wait in microseconds; 0 = 2 s */
   int32_t max_rows_per_task;/* cap on rows of one GEMV task; 0 = 1024 */
+  int32_t trace;            /* 1: record per-task timestamps (see amk_trace_copy) */
 } amk_tuning_t;
 
 typedef struct amk_handle_s* amk_handle_t;
@@ -169,6 +170,26 @@ int amk_reset(amk_handle_t h);
 int amk_set_abort(amk_handle_t h, int32_t value);
 
 const char* amk_status_string(int status);
+
+/* Number of uint64 timestamps per task in a trace record. */
+#define AMK_TRACE_FIELDS 8
+enum {
+  AMK_TRACE_WAIT_BEGIN = 0, /* sync wave starts waiting on the task's counters */
+  AMK_TRACE_WAIT_END = 1,   /* counters satisfied (after the acquire) */
+  AMK_TRACE_INPUT_READY = 2,/* input activation in LDS, streaming waves released */
+  AMK_TRACE_COMPUTE_END = 3,/* every wave finished the task's compute */
+  AMK_TRACE_SIGNALLED = 4,  /* results published, counter incremented */
+  AMK_TRACE_PUBLISHED = 5,  /* result stores issued, before the release fence */
+  AMK_TRACE_RELEASED = 6,   /* release fence done, before the counter increment */
+  AMK_TRACE_SATISFIED = 7   /* counters observed satisfied, before the acquire fence */
+};
+
+/* Copy the per-task timestamps of the last finished step of a handle created
+ * with tuning.trace = 1 into dst[capacity] (host memory), AMK_TRACE_FIELDS
+ * uint64 per task, tasks in amk_schedule_export() order.  Timestamps are the
+ * device's constant 100 MHz wall clock.  Synchronises the handle's stream.
+ * *n_tasks receives the task count.  AMK_ERR_BAD_STATE if tracing is off. */
+int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks);
 
 /* ---- schedule introspection (CPU only, no device needed) -------------------- */
 

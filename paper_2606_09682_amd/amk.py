@@ -31,6 +31,9 @@ AMK_WEIGHTS_W8A16 = 1
 
 AMK_OP_QKV, AMK_OP_ATTN, AMK_OP_COMBINE, AMK_OP_O, AMK_OP_GATEUP, AMK_OP_DOWN, AMK_OP_LMHEAD, AMK_OP_ARGMAX = range(1, 9)
 AMK_MAX_WAITS = 4
+AMK_TRACE_FIELDS = 8
+(AMK_TRACE_WAIT_BEGIN, AMK_TRACE_WAIT_END, AMK_TRACE_INPUT_READY, AMK_TRACE_COMPUTE_END,
+ AMK_TRACE_SIGNALLED, AMK_TRACE_PUBLISHED, AMK_TRACE_RELEASED, AMK_TRACE_SATISFIED) = range(8)
 
 (AMK_CHECK_OK, AMK_CHECK_WELL_FORMED, AMK_CHECK_CAPACITY, AMK_CHECK_WAIT_SATISFIABLE, AMK_CHECK_ALL_JOIN,
  AMK_CHECK_ACYCLIC, AMK_CHECK_QUEUE_ORDER, AMK_CHECK_RACE, AMK_CHECK_KV_ORDER, AMK_CHECK_OUTPUT) = range(10)
@@ -61,7 +64,7 @@ class amk_weights_t(ctypes.Structure):
 
 class amk_tuning_t(ctypes.Structure):
     _fields_ = [("attn_splits", ctypes.c_int32), ("timeout_us", ctypes.c_int32),
-                ("max_rows_per_task", ctypes.c_int32)]
+                ("max_rows_per_task", ctypes.c_int32), ("trace", ctypes.c_int32)]
 
 
 class amk_task_t(ctypes.Structure):
@@ -115,6 +118,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "amk_schedule_check": (ctypes.c_int, [P(amk_config_t), P(amk_tuning_t), ctypes.c_int32, P(amk_task_t),
                                               ctypes.c_int32, ctypes.c_int32, P(amk_check_report_t)]),
         "amk_check_config": (ctypes.c_int, [P(amk_config_t), ctypes.c_int32]),
+        "amk_trace_copy": (ctypes.c_int, [ctypes.c_void_p, P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_int32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -173,6 +177,14 @@ def amk_reset(h) -> None:
 
 def amk_set_abort(h, value: int) -> None:
     _check(load().amk_set_abort(h, int(value)), "amk_set_abort")
+
+
+def amk_trace_copy(h, n_tasks: int):
+    """Per-task timestamps of the last step as a list of AMK_TRACE_FIELDS-tuples."""
+    buf = (ctypes.c_uint64 * (n_tasks * AMK_TRACE_FIELDS))()
+    n = ctypes.c_int32()
+    _check(load().amk_trace_copy(h, buf, len(buf), ctypes.byref(n)), "amk_trace_copy")
+    return [tuple(buf[i * AMK_TRACE_FIELDS:(i + 1) * AMK_TRACE_FIELDS]) for i in range(n.value)]
 
 
 def amk_check_config(cfg: amk_config_t, n_cu: int) -> int:

@@ -220,11 +220,12 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       return AMK_ERR_SCHEDULE_REJECTED;
     }
 
-    // LDS: activation vector (padded to a whole int8 granule) + partials / attention scratch
+    // LDS: activation vector (padded to a whole int8 granule), norm gain,
+    // static per-row data, residual rows, partials / attention scratch
     const int nsw = amk_internal_threads() / 64 - 1;
     const size_t act = round_up((size_t)std::max({s.H, s.nq * s.hd, s.I}), 1024);
     const size_t scr = std::max<size_t>((size_t)nsw * s.max_jobs, (size_t)amk_internal_attn_scratch(s.group, s.hd));
-    const size_t lds_bytes = (act + scr) * 4;
+    const size_t lds_bytes = (act + s.H + 3 * (size_t)s.max_jobs + scr) * 4;
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
       free_handle(h);
@@ -235,12 +236,12 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       free_handle(h);
       return AMK_ERR_UNSUPPORTED;
     }
-    if (amk_internal_prepare(s.group, (int)lds_bytes) != AMK_OK) {
+    if (amk_internal_prepare(s.hd, s.group, (int)lds_bytes) != AMK_OK) {
       free_handle(h);
       return AMK_ERR_DEVICE;
     }
     int per_cu = 0;
-    if (amk_internal_occupancy(s.group, (int)lds_bytes, &per_cu) != AMK_OK || per_cu < 1) {
+    if (amk_internal_occupancy(s.hd, s.group, (int)lds_bytes, &per_cu) != AMK_OK || per_cu < 1) {
       free_handle(h);
       return AMK_ERR_COOPERATIVE_UNSUPPORTED;
     }
@@ -265,6 +266,8 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     const Region r_abort = take(sizeof(int32_t));
     const Region r_tasks = take(sizeof(amk_task_t) * h->sch.tasks.size());
     const Region r_queue = take(sizeof(int32_t) * h->sch.queue_start.size());
+    const bool tracing = tuning && tuning->trace;
+    const Region r_trace = take(tracing ? sizeof(uint64_t) * AMK_TRACE_FIELDS * h->sch.tasks.size() : 0);
     if (hipMalloc(&h->d_block, top) != hipSuccess) {
       h->d_block = nullptr;
       free_handle(h);
@@ -354,6 +357,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.dev_abort = (int32_t*)(base + r_abort.off);
     m.host_status = d_status;
     m.host_abort = d_hab;
+    m.trace = tracing ? (uint64_t*)(base + r_trace.off) : nullptr;
     m.tasks = (const amk_task_t*)(base + r_tasks.off);
     m.queue_start = (const int32_t*)(base + r_queue.off);
     m.lds_act = (int32_t)act;
@@ -421,6 +425,19 @@ int amk_reset(amk_handle_t h) {
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
   *(volatile int32_t*)h->h_status = 0;
   h->epoch = 0;
+  return AMK_OK;
+}
+
+int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks) {
+  if (!h || !dst) return AMK_ERR_INVALID_ARGUMENT;
+  if (!h->dm.trace) return AMK_ERR_BAD_STATE;
+  const size_t n = h->sch.tasks.size();
+  if (n_tasks) *n_tasks = (int32_t)n;
+  if (capacity < (int64_t)(n * AMK_TRACE_FIELDS)) return AMK_ERR_INVALID_ARGUMENT;
+  DeviceGuard guard(h->device);
+  if (h->launched && hipStreamSynchronize((hipStream_t)h->last_stream) != hipSuccess) return AMK_ERR_DEVICE;
+  if (hipMemcpy(dst, h->dm.trace, n * AMK_TRACE_FIELDS * sizeof(uint64_t), hipMemcpyDeviceToHost) != hipSuccess)
+    return AMK_ERR_DEVICE;
   return AMK_OK;
 }
 

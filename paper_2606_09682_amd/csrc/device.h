@@ -53,12 +53,14 @@ struct DevModel {
   int32_t* dev_abort;        // device word: nonzero stops every workgroup at its next wait
   int32_t* host_status;      // host-mapped: first device error code
   const int32_t* host_abort; // host-mapped: raised by amk_set_abort
+  uint64_t* trace;           // [n_tasks][AMK_TRACE_FIELDS] timestamps, or null
   const amk_task_t* tasks;   // sorted by (cu, seq)
   const int32_t* queue_start;// [n_cu + 1]
-  // LDS layout (floats)
+  // LDS layout (floats): act[lds_act] gain[H] stat[2 * part_stride]
+  // res[part_stride] part[lds_scr]
   int32_t lds_act;           // activation vector region (padded to 1024, zero-filled tail)
-  int32_t part_stride;       // GEMV partials per streaming wave (max rows per task)
-  int32_t lds_scr;           // floats after the activation: GEMV partials or attention scratch
+  int32_t part_stride;       // rows of one GEMV task at most (partials per streaming wave)
+  int32_t lds_scr;           // GEMV partials of all streaming waves, or attention scratch
   int32_t lds_bytes;         // dynamic LDS bytes of one workgroup
 };
 
@@ -68,7 +70,7 @@ extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos
 // Threads per workgroup and LDS the kernel needs beyond the model-dependent regions.
 extern "C" int amk_internal_threads(void);
 extern "C" int amk_internal_attn_scratch(int group, int head_dim);
-extern "C" int amk_internal_prepare(int group, int lds_bytes);
-extern "C" int amk_internal_occupancy(int group, int lds_bytes, int* blocks_per_cu);
+extern "C" int amk_internal_prepare(int head_dim, int group, int lds_bytes);
+extern "C" int amk_internal_occupancy(int head_dim, int group, int lds_bytes, int* blocks_per_cu);
 
 }  // namespace amk

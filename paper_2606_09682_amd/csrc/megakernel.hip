@@ -4,17 +4,31 @@
 // through monotonic counters (paper §4 "Synchronization model").
 //
 // Workgroup layout (512 threads = 8 wave64s):
-//   wave 0      "sync wave": waits on counters (agent-scope acquire), moves the
-//               task's input activation into LDS (RMSNorm folded in), writes
-//               every result other CUs read, then releases and signals.
+//   wave 0      "sync wave": waits on counters (agent-scope acquire), reduces
+//               the streaming waves' partial row sums, applies the fused
+//               epilogue (RMSNorm scale, RoPE + KV append, SwiGLU, residual,
+//               int8 row scale, argmax), writes every result other CUs read,
+//               then releases and signals.
 //   waves 1..7  "streaming waves": stream the task's weight rows from HBM in
 //               16-byte-per-lane vectors through a double-buffered register
 //               pipeline and reduce them against the LDS activation.
-// The streaming waves issue the first weight loads of a task BEFORE the
-// workgroup barrier that publishes the task's input, so HBM keeps streaming
-// while the sync wave waits for producers on other CUs.  Only the sync wave
-// executes agent-scope acquire/release sequences, whose vmcnt(0) drains would
-// otherwise stall the streaming waves' in-flight loads.
+//   all waves   load the task's input activation into LDS after the wait (one
+//               round trip) and run the attention tasks.
+//
+// Per task the workgroup passes four barriers:
+//   B1a  the sync wave's counter wait is satisfied (or the launch aborts)
+//   B1b  the input activation is in LDS
+//   B2   the task's compute is done (partials / attention output in LDS)
+//   B3   the sync wave has issued the task's result stores
+// The streaming waves issue the weight loads of their NEXT task right after
+// B3.  Memory requests of one CU are served roughly in order, so loads issued
+// before the result stores would delay the release and hence every consumer
+// on other CUs; issued after them, the loads stream while the counters
+// propagate and the next input is fetched.
+//
+// Only the sync wave executes agent-scope acquire/release sequences: their
+// vmcnt(0) drains would otherwise stall the streaming waves' in-flight loads.
+// Lane reductions use DPP (VALU latency) rather than LDS permutes.
 //
 // No MFMA: a batch-1 GEMV is a matrix-vector product, bound by HBM bandwidth.
 #include <hip/hip_runtime.h>
@@ -33,12 +47,13 @@ constexpr int PIPE = 8;       // 1-KiB granules per pipeline half, per wave
 constexpr int GRAN = 1024;    // bytes per wave-wide 16-B-per-lane load
 
 struct Ctl {
-  float rs;          // 1 / sqrt(mean(x^2) + eps) of the task input
   int abort;
+  int res_buf, res_lo, res_hi;  // residual rows cached in LDS: x buffer index and row range
   float m_run[8], l_run[8], alpha[8];
+  float ssq[NW];                // per-wave sum of squares of the task input
 };
 
-// ---------------------------------------------------------------- helpers
+// ---------------------------------------------------------------- memory helpers
 // Pointers read out of the model record are generic; casting them to the
 // global (1) or constant (4) address space makes the compiler emit global_*
 // vector accesses and scalar s_load reads instead of flat accesses, which
@@ -70,6 +85,7 @@ __device__ __forceinline__ T ldc(const void* p) {
   return __builtin_bit_cast(T, *(const AMK_CONST B*)p);
 }
 
+// ---------------------------------------------------------------- numeric helpers
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ float bf16f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
@@ -79,22 +95,58 @@ __device__ __forceinline__ uint16_t f2bf(float f) {  // round to nearest even
   return (uint16_t)(u >> 16);
 }
 __device__ __forceinline__ float i8f(uint32_t w, int k) { return (float)(int8_t)(w >> (8 * k)); }
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+// DPP lane moves.  Control codes: quad_perm [1,0,3,2] = 0xb1, [2,3,0,1] = 0x4e,
+// row_mirror = 0x140, row_half_mirror = 0x141, row_bcast15 = 0x142,
+// row_bcast31 = 0x143.  Lanes outside row_mask receive 0.
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, false));
+}
+
+// Sum over groups of N consecutive lanes (N in 2, 4, 8, 16, 32); every lane of
+// a group receives its group's sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16 || N == 32, "group size");
+  v += dpp<0xb1>(v);
+  if constexpr (N >= 4) v += dpp<0x4e>(v);
+  if constexpr (N >= 8) v += dpp<0x141>(v);
+  if constexpr (N >= 16) v += dpp<0x140>(v);
+  if constexpr (N >= 32) v += __shfl_xor(v, 16);
   return v;
+}
+template <int N>
+__device__ __forceinline__ float group_max(float v) {
+  v = fmaxf(v, dpp<0xb1>(v));
+  if constexpr (N >= 4) v = fmaxf(v, dpp<0x4e>(v));
+  if constexpr (N >= 8) v = fmaxf(v, dpp<0x141>(v));
+  if constexpr (N >= 16) v = fmaxf(v, dpp<0x140>(v));
+  if constexpr (N >= 32) v = fmaxf(v, __shfl_xor(v, 16));
+  return v;
+}
+
+// Full-wave sum / max, returned to every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum<16>(v);
+  v += dpp<0x142, 0xa>(v);  // rows 1, 3 += last lane of rows 0, 2
+  v += dpp<0x143, 0xc>(v);  // rows 2, 3 += lane 31
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  v = group_max<16>(v);
+  v = fmaxf(v, __shfl_xor(v, 16));
+  v = fmaxf(v, __shfl_xor(v, 32));
   return v;
 }
-__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 __device__ __forceinline__ bool is_gemv(int op) {
   return op == AMK_OP_QKV || op == AMK_OP_O || op == AMK_OP_GATEUP || op == AMK_OP_DOWN ||
          op == AMK_OP_LMHEAD;
+}
+__device__ __forceinline__ bool is_normed(int op) {
+  return op == AMK_OP_QKV || op == AMK_OP_GATEUP || op == AMK_OP_LMHEAD;
 }
 
 // ---------------------------------------------------------------- GEMV task geometry
@@ -134,23 +186,24 @@ __device__ __forceinline__ const float* mat_scale(const DevModel& m, const amk_t
   if (mat < 0) return m.lm_s;
   return ldc<const float*>(&m.layers[t.layer].s[mat]);
 }
-__device__ __forceinline__ float scale_of(const DevModel& m, const amk_task_t& t, int mat, int row) {
-  return ldg<float>(mat_scale(m, t, mat) + row);
-}
 
 __device__ __forceinline__ int task_jobs_dev(const amk_task_t& t) {
   const int n = t.end - t.begin;
   return (t.op == AMK_OP_QKV || t.op == AMK_OP_GATEUP) ? 2 * n : n;
 }
 
+__device__ __forceinline__ int task_k(const DevModel& m, const amk_task_t& t) {
+  switch (t.op) {
+    case AMK_OP_O: return m.nq * m.hd;
+    case AMK_OP_DOWN: return m.I;
+    case AMK_OP_ATTN: return m.group * m.hd;
+    default: return m.H;
+  }
+}
+
 __device__ __forceinline__ Gemv gemv_geom(const DevModel& m, const amk_task_t& t) {
   Gemv g;
-  int K;
-  switch (t.op) {
-    case AMK_OP_O: K = m.nq * m.hd; break;
-    case AMK_OP_DOWN: K = m.I; break;
-    default: K = m.H; break;
-  }
+  const int K = task_k(m, t);
   g.int8 = (t.op == AMK_OP_LMHEAD) ? m.lm_int8 : (m.fmt == AMK_WEIGHTS_W8A16);
   g.row_bytes = g.int8 ? K : 2 * K;
   g.gpr = (g.row_bytes + GRAN - 1) / GRAN;
@@ -262,9 +315,9 @@ __device__ __forceinline__ void consume_block(const uint4 (&buf)[PIPE], int& j, 
   }
 }
 
-// ---------------------------------------------------------------- sync wave: waits
+// ---------------------------------------------------------------- sync wave: counters
 __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t, const amk_task_t* tp, uint32_t epoch,
-                          uint64_t timeout_ticks, int lane) {
+                                          uint64_t timeout_ticks, int lane, uint64_t* tr) {
   const int nw = t.n_wait;
   if (nw == 0) return __hip_atomic_load(m.dev_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
   uint32_t* p = nullptr;
@@ -298,75 +351,148 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
         return false;
       }
     }
-    __builtin_amdgcn_s_sleep(2);
+    __builtin_amdgcn_s_sleep(1);
   }
+  if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SATISFIED, (uint64_t)wall_clock64());
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   return true;
 }
 
-__device__ __forceinline__ void signal_done(const DevModel& m, const amk_task_t& t, int lane) {
+__device__ __forceinline__ void release_signal(const DevModel& m, int counter, int lane) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  if (lane == 0 && t.signal_counter >= 0)
-    __hip_atomic_fetch_add(m.counters + (size_t)t.signal_counter * kCounterStride, 1u, __ATOMIC_RELAXED,
+  if (lane == 0 && counter >= 0)
+    __hip_atomic_fetch_add(m.counters + (size_t)counter * kCounterStride, 1u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// ---------------------------------------------------------------- sync wave: prologues
-// act[k] = x[k] * g[k] and ctl.rs = 1/sqrt(mean(x^2) + eps); the GEMV result
-// is scaled by rs in the epilogue (RMSNorm folded into the consumer).
-template <bool SRC_BF16>
-__device__ __forceinline__ void load_normed(const void* src, const uint16_t* g, int K, float eps, float* act, Ctl& ctl, int lane) {
-  constexpr int NB = 8;
-  float ss = 0.f;
-  for (int b = 0; b < K; b += NB * 256) {
-    float4 xv[NB];
-    uint2 gv[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int e = b + (i * 64 + lane) * 4;
-      if (e < K) {
-        if (SRC_BF16) {
-          const uint2 r = ldg<uint2>((const uint16_t*)src + e);
-          xv[i] = make_float4(bf_lo(r.x), bf_hi(r.x), bf_lo(r.y), bf_hi(r.y));
-        } else {
-          xv[i] = ldg<float4>((const float*)src + e);
-        }
-        gv[i] = ldg<uint2>(g + e);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int e = b + (i * 64 + lane) * 4;
-      if (e < K) {
-        const float4 x = xv[i];
-        ss = fmaf(x.x, x.x, ss); ss = fmaf(x.y, x.y, ss); ss = fmaf(x.z, x.z, ss); ss = fmaf(x.w, x.w, ss);
-        const float4 o = make_float4(x.x * bf_lo(gv[i].x), x.y * bf_hi(gv[i].x), x.z * bf_lo(gv[i].y),
-                                     x.w * bf_hi(gv[i].y));
-        *reinterpret_cast<float4*>(act + e) = o;
-      }
+// ---------------------------------------------------------------- static per-task data
+// Data that does not depend on this launch's results (norm gains, RoPE
+// factors, int8 row scales, the layer-0 embedding rows) is fetched before
+// the task's counter wait, so the critical path after the wait only moves the
+// input activation.  LDS regions after the activation:
+//   gain[H]                 RMSNorm gain of a normed input, fp32
+//   stat[2 * max_rows]      int8 row scales (rows [0, nj)), then for QKV the
+//                           RoPE (cos, sin) of unit u at [nj + 2u, nj + 2u + 1]
+//   res[max_rows]           residual rows of the last O / down task (or the
+//                           layer-0 embedding rows)
+//   part[...]               per-streaming-wave row partials / attention scratch
+struct Lds {
+  float* act;
+  float* gain;
+  float* stat;
+  float* res;
+  float* part;
+};
+
+__device__ __forceinline__ void load_static(const DevModel& m, const amk_task_t& t, int token, int pos,
+                                            const Lds& L, Ctl& ctl, int lane) {
+  const int op = t.op;
+  if (is_normed(op)) {
+    const uint16_t* g = op == AMK_OP_QKV ? ldc<const uint16_t*>(&m.layers[t.layer].attn_norm)
+                        : op == AMK_OP_GATEUP ? ldc<const uint16_t*>(&m.layers[t.layer].mlp_norm)
+                                              : m.final_norm;
+    for (int e = lane * 8; e < m.H; e += 512) {
+      const uint4 w = ldg<uint4>(g + e);
+      *reinterpret_cast<float4*>(L.gain + e) = make_float4(bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y));
+      *reinterpret_cast<float4*>(L.gain + e + 4) = make_float4(bf_lo(w.z), bf_hi(w.z), bf_lo(w.w), bf_hi(w.w));
     }
   }
-  ss = wave_sum(ss);
-  if (lane == 0) ctl.rs = 1.0f / sqrtf(ss / (float)K + eps);
+  if (!is_gemv(op)) return;
+  const Gemv g = gemv_geom(m, t);
+  if (g.int8) {
+    for (int j = lane; j < g.nj; j += 64) {
+      int mat, row;
+      job_row(m, t, j, &mat, &row);
+      L.stat[j] = ldg<float>(mat_scale(m, t, mat) + row);
+    }
+  }
+  if (op == AMK_OP_QKV) {
+    const int nu = t.end - t.begin;
+    for (int u = lane; u < nu; u += 64) {
+      const int i = (t.begin + u) & (m.half - 1);
+      const float2 cs = ldg<float2>(m.rope + (size_t)pos * m.half + i);
+      L.stat[g.nj + 2 * u] = cs.x;
+      L.stat[g.nj + 2 * u + 1] = cs.y;
+    }
+  }
+  if (op == AMK_OP_O && t.layer == 0) {
+    const uint16_t* e = m.embed + (size_t)token * m.H;
+    for (int r = t.begin + lane; r < t.end; r += 64) L.res[r - t.begin] = bf16f(ldg<uint16_t>(e + r));
+    if (lane == 0) {
+      ctl.res_buf = 0;
+      ctl.res_lo = t.begin;
+      ctl.res_hi = t.end;
+    }
+  }
 }
 
-// Plain fp32 copy global -> LDS, 16 vectors of 16 B in flight per lane.
-__device__ __forceinline__ void load_plain(const float* src, int K, float* act, int lane) {
-  constexpr int NB = 16;
-  const int n16 = K / 4;  // 16-byte vectors; K is a multiple of 4
-  for (int b = 0; b < n16; b += NB * 64) {
-    float4 v[NB];
+// ---------------------------------------------------------------- input activation (all waves)
+// The task input moves into LDS in one round trip: wave w copies a 1/8 slice.
+// Normed inputs store x * gain and leave each wave's sum of x^2 in ctl.ssq;
+// the GEMV result is scaled by 1/sqrt(mean(x^2) + eps) in the epilogue
+// (RMSNorm folded into the consumer).
+__device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& t, int token, const Lds& L, Ctl& ctl,
+                                           int wave, int lane) {
+  const int op = t.op;
+  const float* src = nullptr;
+  const uint16_t* src_bf = nullptr;
+  switch (op) {
+    case AMK_OP_QKV:
+      if (t.layer == 0) src_bf = m.embed + (size_t)token * m.H;
+      else src = m.x + (size_t)(2 * t.layer) * m.H;
+      break;
+    case AMK_OP_GATEUP: src = m.x + (size_t)(2 * t.layer + 1) * m.H; break;
+    case AMK_OP_LMHEAD: src = m.x + (size_t)(2 * m.L) * m.H; break;
+    case AMK_OP_O: src = m.o + (size_t)t.layer * m.nq * m.hd; break;
+    case AMK_OP_DOWN: src = m.a + (size_t)t.layer * m.I; break;
+    case AMK_OP_ATTN: src = m.q + (size_t)t.layer * m.nq * m.hd + (size_t)t.aux * m.group * m.hd; break;
+    default: return;
+  }
+  const int K = task_k(m, t);
+  const int n4 = K >> 2;  // float4 vectors (K is a multiple of 16)
+  const int v0 = (n4 * wave) / NW, v1 = (n4 * (wave + 1)) / NW;
+  const bool normed = is_normed(op);
+  float ss = 0.f;
+  constexpr int NB = 8;
+  for (int b = v0; b < v1; b += NB * 64) {
+    float4 xv[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      const int e = b + i * 64 + lane;
-      if (e < n16) v[i] = ldg<float4>(src + (size_t)e * 4);
+      const int v = b + i * 64 + lane;
+      if (v < v1) {
+        if (src_bf) {
+          const uint2 r = ldg<uint2>(src_bf + (size_t)v * 4);
+          xv[i] = make_float4(bf_lo(r.x), bf_hi(r.x), bf_lo(r.y), bf_hi(r.y));
+        } else {
+          xv[i] = ldg<float4>(src + (size_t)v * 4);
+        }
+      }
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      const int e = b + i * 64 + lane;
-      if (e < n16) *reinterpret_cast<float4*>(act + (size_t)e * 4) = v[i];
+      const int v = b + i * 64 + lane;
+      if (v < v1) {
+        float4 x = xv[i];
+        if (normed) {
+          ss = fmaf(x.x, x.x, ss); ss = fmaf(x.y, x.y, ss); ss = fmaf(x.z, x.z, ss); ss = fmaf(x.w, x.w, ss);
+          const float4 g = *reinterpret_cast<const float4*>(L.gain + v * 4);
+          x = make_float4(x.x * g.x, x.y * g.y, x.z * g.z, x.w * g.w);
+        }
+        *reinterpret_cast<float4*>(L.act + v * 4) = x;
+      }
     }
   }
+  if (normed) {
+    ss = wave_sum(ss);
+    if (lane == 0) ctl.ssq[wave] = ss;
+  }
+}
+
+__device__ __forceinline__ float input_rs(const DevModel& m, const Ctl& ctl) {
+  float ss = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) ss += ctl.ssq[w];
+  return 1.0f / sqrtf(ss / (float)m.H + m.eps);
 }
 
 // ---------------------------------------------------------------- row sums of a GEMV task
@@ -383,26 +509,24 @@ __device__ __forceinline__ float row_sum(const float* part, int stride, const Ge
 }
 
 // ---------------------------------------------------------------- sync wave: epilogues
-__device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, const Gemv& g, const float* part, int pos,
-                        uint16_t* kv, float rs, int lane) {
+__device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L, int pos,
+                                        uint16_t* kv, float rs, int lane) {
   const int l = t.layer;
   for (int u = t.begin + lane; u < t.end; u += 64) {
     const int j0 = 2 * (u - t.begin);
-    float y0 = row_sum(part, m.part_stride, g, j0) * rs;
-    float y1 = row_sum(part, m.part_stride, g, j0 + 1) * rs;
-    int mat, r0, r1;
-    job_row(m, t, j0, &mat, &r0);
-    job_row(m, t, j0 + 1, &mat, &r1);
+    float y0 = row_sum(L.part, m.part_stride, g, j0) * rs;
+    float y1 = row_sum(L.part, m.part_stride, g, j0 + 1) * rs;
     if (g.int8) {
-      y0 *= scale_of(m, t, mat, r0);
-      y1 *= scale_of(m, t, mat, r1);
+      y0 *= L.stat[j0];
+      y1 *= L.stat[j0 + 1];
     }
     const int hh = u >> m.half_log2;
     const int i = u & (m.half - 1);
+    const int mat = hh < m.nq ? W_Q : hh < m.nq + m.nkv ? W_K : W_V;
     if (mat != W_V) {
-      const float2 cs = ldg<float2>(m.rope + (size_t)pos * m.half + i);
-      const float a = y0 * cs.x - y1 * cs.y;
-      const float b = y1 * cs.x + y0 * cs.y;
+      const float c = L.stat[g.nj + 2 * (u - t.begin)], s = L.stat[g.nj + 2 * (u - t.begin) + 1];
+      const float a = y0 * c - y1 * s;
+      const float b = y1 * c + y0 * s;
       y0 = a;
       y1 = b;
     }
@@ -420,40 +544,50 @@ __device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, 
   }
 }
 
-__device__ __forceinline__ void epi_rows(const DevModel& m, const amk_task_t& t, const Gemv& g, const float* part, float rs,
-                         float* logits, int lane) {
-  const int l = t.layer;
-  const int stride = m.part_stride;
-  if (t.op == AMK_OP_GATEUP) {
-    for (int r = t.begin + lane; r < t.end; r += 64) {
-      const int j = 2 * (r - t.begin);
-      float gv = row_sum(part, stride, g, j) * rs;
-      float uv = row_sum(part, stride, g, j + 1) * rs;
-      if (g.int8) {
-        gv *= scale_of(m, t, W_G, r);
-        uv *= scale_of(m, t, W_U, r);
-      }
-      const float silu = gv / (1.0f + __expf(-gv));
-      stg<float>(m.a + (size_t)l * m.I + r, silu * uv);
-    }
-    return;
+// O and down projections: x_out = x_in + W y, with x_in rows taken from LDS
+// when this workgroup's previous residual task produced exactly those rows.
+__device__ __forceinline__ void epi_residual(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L,
+                                             Ctl& ctl, int lane) {
+  const int xin = t.op == AMK_OP_O ? 2 * t.layer : 2 * t.layer + 1;
+  const bool cached = ctl.res_buf == xin && ctl.res_lo == t.begin && ctl.res_hi == t.end;
+  for (int r = t.begin + lane; r < t.end; r += 64) {
+    float y = row_sum(L.part, m.part_stride, g, r - t.begin);
+    if (g.int8) y *= L.stat[r - t.begin];
+    const float x = cached ? L.res[r - t.begin] : ldg<float>(m.x + (size_t)xin * m.H + r);
+    const float o = x + y;
+    stg<float>(m.x + (size_t)(xin + 1) * m.H + r, o);
+    L.res[r - t.begin] = o;
   }
-  if (t.op == AMK_OP_O || t.op == AMK_OP_DOWN) {
-    const int mat = t.op == AMK_OP_O ? W_O : W_D;
-    const int xin = t.op == AMK_OP_O ? 2 * l : 2 * l + 1;
-    for (int r = t.begin + lane; r < t.end; r += 64) {
-      float y = row_sum(part, stride, g, r - t.begin);
-      if (g.int8) y *= scale_of(m, t, mat, r);
-      stg<float>(m.x + (size_t)(xin + 1) * m.H + r, ldg<float>(m.x + (size_t)xin * m.H + r) + y);
-    }
-    return;
+  if (lane == 0) {
+    ctl.res_buf = xin + 1;
+    ctl.res_lo = t.begin;
+    ctl.res_hi = t.end;
   }
-  // LM head: logits + per-task argmax partial (lowest index on ties)
+}
+
+__device__ __forceinline__ void epi_gateup(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L,
+                                           float rs, int lane) {
+  for (int r = t.begin + lane; r < t.end; r += 64) {
+    const int j = 2 * (r - t.begin);
+    float gv = row_sum(L.part, m.part_stride, g, j) * rs;
+    float uv = row_sum(L.part, m.part_stride, g, j + 1) * rs;
+    if (g.int8) {
+      gv *= L.stat[j];
+      uv *= L.stat[j + 1];
+    }
+    const float silu = gv / (1.0f + __expf(-gv));
+    stg<float>(m.a + (size_t)t.layer * m.I + r, silu * uv);
+  }
+}
+
+// LM head: logits + per-task argmax partial (lowest index on ties).
+__device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L,
+                                           float rs, float* logits, int lane) {
   float best = -INFINITY;
   int besti = 0x7fffffff;
   for (int r = t.begin + lane; r < t.end; r += 64) {
-    float y = row_sum(part, stride, g, r - t.begin) * rs;
-    if (g.int8) y *= ldg<float>(m.lm_s + r);
+    float y = row_sum(L.part, m.part_stride, g, r - t.begin) * rs;
+    if (g.int8) y *= L.stat[r - t.begin];
     stg<float>(logits + r, y);
     if (y > best || (y == best && r < besti)) { best = y; besti = r; }
   }
@@ -466,26 +600,13 @@ __device__ __forceinline__ void epi_rows(const DevModel& m, const amk_task_t& t,
   if (lane == 0) stg<float2>(m.argp + 2 * t.aux, make_float2(best, __int_as_float(besti)));
 }
 
-// x1 = x0 + Wo o at layer 0 needs the gathered embedding row as x0.
-__device__ __forceinline__ void epi_o_layer0(const DevModel& m, const amk_task_t& t, const Gemv& g, const float* part, int token,
-                             int lane) {
-  const int stride = m.part_stride;
-  const uint16_t* e = m.embed + (size_t)token * m.H;
-  for (int r = t.begin + lane; r < t.end; r += 64) {
-    float y = row_sum(part, stride, g, r - t.begin);
-    if (g.int8) y *= scale_of(m, t, W_O, r);
-    stg<float>(m.x + (size_t)1 * m.H + r, bf16f(ldg<uint16_t>(e + r)) + y);
-  }
-}
-
-// Merge the position splits of query heads [begin, end) (flash-decoding style).
-__device__ __forceinline__ void combine(const DevModel& m, const amk_task_t& t, int pos, int lane) {
-  const int l = t.layer;
+// Merge the position splits of query heads [h0, h1) (flash-decoding style).
+__device__ __forceinline__ void combine_heads(const DevModel& m, int l, int h0, int h1, int pos, int lane) {
   const int n_pos = pos + 1;
   const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
   const int active = (n_pos + chunk - 1) / chunk;
   const int rec = m.group * (kPartHead + m.hd);
-  for (int h = t.begin; h < t.end; ++h) {
+  for (int h = h0; h < h1; ++h) {
     const int g = h / m.group, hg = h - g * m.group;
     const float* base = m.part + ((size_t)(l * m.nkv + g) * m.nsplit) * rec + hg * (kPartHead + m.hd);
     float ms = -INFINITY, ls = 0.f;
@@ -496,15 +617,12 @@ __device__ __forceinline__ void combine(const DevModel& m, const amk_task_t& t, 
     }
     const float M = wave_max(ms);
     const float w = lane < active ? __expf(ms - M) : 0.f;
-    const float Ls = wave_sum(w * ls);
-    const float inv = 1.0f / Ls;
+    const float inv = 1.0f / wave_sum(w * ls);
     float* dst = m.o + (size_t)l * m.nq * m.hd + (size_t)h * m.hd;
     for (int d = lane; d < m.hd; d += 64) {
       float acc = 0.f;
-      for (int s = 0; s < active; ++s) {
-        const float ws = __shfl(w, s);
-        acc = fmaf(ws, ldg<float>(base + (size_t)s * rec + kPartHead + d), acc);
-      }
+      for (int s = 0; s < active; ++s)
+        acc = fmaf(__shfl(w, s), ldg<float>(base + (size_t)s * rec + kPartHead + d), acc);
       stg<float>(dst + d, acc * inv);
     }
   }
@@ -515,9 +633,8 @@ __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t
   int besti = 0x7fffffff;
   for (int s = t.begin + lane; s < t.end; s += 64) {
     const float2 vi = ldg<float2>(m.argp + 2 * s);
-    const float v = vi.x;
     const int i = __float_as_int(vi.y);
-    if (v > best || (v == best && i < besti)) { best = v; besti = i; }
+    if (vi.x > best || (vi.x == best && i < besti)) { best = vi.x; besti = i; }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -529,9 +646,24 @@ __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t
 }
 
 // ---------------------------------------------------------------- attention (all 8 waves)
-// Partial attention of query group `t.aux` over position split t.begin of
-// t.end: scores, running max / sum (online softmax) and the V-weighted sum.
-// One K or V row slice of EPL bf16 values per lane.
+// Geometry of the attention split of one task, shared with the host's LDS
+// sizing.  HD: head dim; GM: largest query group handled (accumulators per
+// lane = GM * EPL); EPL: head dims per lane (8 for groups <= 4, 4 for groups
+// <= 8 to halve the accumulators); LPR lanes cover one K/V row, RPW rows per
+// wave-wide load, RP rows per pass of the workgroup, KB rows per lane per
+// sub-chunk of SC rows.
+template <int HD, int GM>
+struct AttnGeom {
+  static constexpr int EPL = GM <= 4 ? 8 : 4;
+  static constexpr int LPR = HD / EPL;
+  static constexpr int RPW = 64 / LPR;
+  static constexpr int RP = NW * RPW;
+  static constexpr int KB = GM <= 4 ? 8 : 4;
+  static constexpr int SC = RP * KB;
+  static constexpr int SCRATCH = GM * SC + NW * GM * HD + GM * HD;  // floats
+  static_assert(LPR >= 2 && LPR <= 32, "lanes per row");
+};
+
 template <int EPL> struct RowVec;
 template <> struct RowVec<8> { uint4 v; };
 template <> struct RowVec<4> { uint2 v; };
@@ -554,41 +686,27 @@ __device__ __forceinline__ float row_elem(const RowVec<EPL>& r, int e) {
   return (e & 1) ? bf_hi(w) : bf_lo(w);
 }
 
-// Geometry of the attention work split (shared with the host LDS sizing).
-// GM: largest query group handled; KB: K/V rows per lane per sub-chunk;
-// EPL: head dims per lane (8 for groups <= 4, 4 for groups <= 8 to halve
-// the per-lane accumulators).
-template <int GM, int KB, int EPL>
-struct AttnGeom {
-  int LPR, RPW, RP, SC;
-  __device__ __forceinline__ explicit AttnGeom(int hd) {
-    LPR = hd / EPL;
-    RPW = 64 / LPR;
-    RP = NW * RPW;
-    SC = RP * KB;
-  }
-};
-
 // Partial attention of query group `t.aux` over position split t.begin of
 // t.end: scores, running max / sum (online softmax) and the V-weighted sum.
-template <int GM, int KB, int EPL>
+// Leaves out[G][HD] (unnormalised) in scratch and (m, l) per head in ctl.
+template <int HD, int GM>
 __device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t, int pos,
                                           const uint16_t* __restrict__ kv, const float* __restrict__ q,
                                           float* __restrict__ scr, Ctl& ctl, int wave, int lane) {
-  const int G = m.group, hd = m.hd;
+  using A = AttnGeom<HD, GM>;
+  constexpr int EPL = A::EPL, LPR = A::LPR, RPW = A::RPW, RP = A::RP, KB = A::KB, SC = A::SC;
+  const int G = m.group;
   const int n_pos = pos + 1;
   const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
   const int j0 = t.begin * chunk;
   const int j1 = min(n_pos, j0 + chunk);
-  const AttnGeom<GM, KB, EPL> ag(hd);
-  const int LPR = ag.LPR, RPW = ag.RPW, RP = ag.RP, SC = ag.SC;
-  const int sub = lane / LPR, c = lane - sub * LPR;
-  const size_t hs = (size_t)m.max_seq * hd;
+  const int sub = lane / LPR, c = lane % LPR;
+  const size_t hs = (size_t)m.max_seq * HD;
   const uint16_t* Kp = kv + ((size_t)(t.layer * 2 + 0) * m.nkv + t.aux) * hs + c * EPL;
   const uint16_t* Vp = kv + ((size_t)(t.layer * 2 + 1) * m.nkv + t.aux) * hs + c * EPL;
-  float* sc = scr;                        // [GM][SC]
-  float* red = scr + GM * SC;             // [NW][G][hd]
-  float* out = red + NW * G * hd;         // [G][hd]
+  float* sc = scr;                  // [GM][SC]
+  float* red = scr + GM * SC;       // [NW][GM][HD]
+  float* out = red + NW * GM * HD;  // [G][HD]
 
   if (threadIdx.x < 8) {
     ctl.m_run[threadIdx.x] = -INFINITY;
@@ -608,7 +726,7 @@ __device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t
     for (int k = 0; k < KB; ++k) {
       const int r = wave * RPW + sub + k * RP;
       zero_row<EPL>(kr[k]);
-      if (r < n) kr[k] = load_row<EPL>(Kp + (size_t)(t0 + r) * hd);
+      if (r < n) kr[k] = load_row<EPL>(Kp + (size_t)(t0 + r) * HD);
     }
     // scores s_j = q_h . k_j / sqrt(d) for the group's query heads
 #pragma unroll
@@ -617,11 +735,11 @@ __device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t
 #pragma unroll
       for (int h = 0; h < GM; ++h) {
         if (h < G) {
-          const float* qh = q + h * hd + c * EPL;
+          const float* qh = q + h * HD + c * EPL;
           float d = 0.f;
 #pragma unroll
           for (int e = 0; e < EPL; ++e) d = fmaf(row_elem<EPL>(kr[k], e), qh[e], d);
-          for (int o = 1; o < LPR; o <<= 1) d += __shfl_xor(d, o);
+          d = group_sum<LPR>(d);
           if (c == 0 && r < n) sc[h * SC + r] = d * m.attn_scale;
         }
       }
@@ -631,7 +749,7 @@ __device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t
     for (int k = 0; k < KB; ++k) {
       const int r = wave * RPW + sub + k * RP;
       zero_row<EPL>(vr[k]);
-      if (r < n) vr[k] = load_row<EPL>(Vp + (size_t)(t0 + r) * hd);
+      if (r < n) vr[k] = load_row<EPL>(Vp + (size_t)(t0 + r) * HD);
     }
     __syncthreads();
     // running max / sum per head (wave h handles head h)
@@ -682,132 +800,134 @@ __device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t
     }
     __syncthreads();
   }
-  // reduce over the rows a wave covers (lanes with equal c), then over waves
+  // reduce over the row groups of a wave (lanes with equal c), then over waves
 #pragma unroll
   for (int h = 0; h < GM; ++h) {
     if (h < G) {
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         float v = acc[h][e];
+#pragma unroll
         for (int o = LPR; o < 64; o <<= 1) v += __shfl_xor(v, o);
-        if (sub == 0) red[(wave * G + h) * hd + c * EPL + e] = v;
+        if (sub == 0) red[(wave * GM + h) * HD + c * EPL + e] = v;
       }
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < G * hd; i += NT) {
+  for (int i = threadIdx.x; i < G * HD; i += NT) {
+    const int h = i / HD, d = i - h * HD;
     float s = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) s += red[w * G * hd + i];
+    for (int w = 0; w < NW; ++w) s += red[(w * GM + h) * HD + d];
     out[i] = s;
   }
 }
 
-template <int GM, int KB, int EPL>
+template <int HD, int GM>
 __device__ __forceinline__ void epi_attn(const DevModel& m, const amk_task_t& t, const float* scr, const Ctl& ctl,
                                          int pos, int lane) {
-  const int G = m.group, hd = m.hd;
+  using A = AttnGeom<HD, GM>;
+  const int G = m.group;
   const int n_pos = pos + 1;
   const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
   if (t.begin * chunk >= n_pos) return;  // empty split: the combine ignores it
-  const AttnGeom<GM, KB, EPL> ag(hd);
-  const float* out = scr + GM * ag.SC + NW * G * hd;
-  const int rec = G * (kPartHead + hd);
+  const float* out = scr + GM * A::SC + NW * GM * HD;
+  const int rec = G * (kPartHead + HD);
   float* dst = m.part + ((size_t)(t.layer * m.nkv + t.aux) * m.nsplit + t.begin) * rec;
   for (int h = 0; h < G; ++h) {
-    float* d = dst + h * (kPartHead + hd);
+    float* d = dst + h * (kPartHead + HD);
     if (lane == 0) stg<float2>(d, make_float2(ctl.m_run[h], ctl.l_run[h]));
-    for (int e = lane; e < hd; e += 64) stg<float>(d + kPartHead + e, out[h * hd + e]);
+    for (int e = lane; e < HD; e += 64) stg<float>(d + kPartHead + e, out[h * HD + e]);
   }
 }
 
 // ---------------------------------------------------------------- the kernel
-// GM / KB / EPL: attention geometry (see attention()); one instantiation per
-// query-group class keeps each kernel's register allocation independent.
-template <int GM, int KB, int EPL>
+template <int HD, int GM>
 __global__ void __launch_bounds__(NT, 1)
 amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16_t* __restrict__ kv,
                   float* __restrict__ logits, uint64_t timeout_ticks) {
   extern __shared__ float4 lds4[];
-  float* act = reinterpret_cast<float*>(lds4);
-  float* part = act + m.lds_act;
   __shared__ Ctl ctl;
+  Lds L;
+  L.act = reinterpret_cast<float*>(lds4);
+  L.gain = L.act + m.lds_act;
+  L.stat = L.gain + m.H;
+  L.res = L.stat + 2 * m.part_stride;
+  L.part = L.res + m.part_stride;
 
   const int wave = uni(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int pstride = m.part_stride;
 
-  for (int i = threadIdx.x; i < m.lds_act; i += NT) act[i] = 0.f;
+  for (int i = threadIdx.x; i < m.lds_act; i += NT) L.act[i] = 0.f;
   if (threadIdx.x == 0) {
     ctl.abort = 0;
-    ctl.rs = 1.f;
+    ctl.res_buf = -1;
+    ctl.res_lo = ctl.res_hi = 0;
+  }
+
+  const int qb = ldc<int32_t>(m.queue_start + blockIdx.x), qe = ldc<int32_t>(m.queue_start + blockIdx.x + 1);
+  // streaming state carried from one task to the next (the weight loads of
+  // task idx are issued at the end of task idx - 1)
+  uint4 bufA[PIPE], bufB[PIPE];
+  Cursor ic;
+  int gi = 0, g0 = 0, g1 = 0;
+
+  auto prefetch = [&](int idx) {
+    g0 = g1 = gi = 0;
+    if (idx >= qe) return;
+    const amk_task_t tn = ldc<amk_task_t>(m.tasks + idx);
+    if (!is_gemv(tn.op)) return;
+    const Gemv gn = gemv_geom(m, tn);
+    const int sw = wave - 1;
+    g0 = wave_gbegin(gn.G, sw);
+    g1 = wave_gbegin(gn.G, sw + 1);
+    gi = g0;
+    if (g0 < g1) {
+      cursor_init(ic, m, tn, gn, g0);
+      issue_block(bufA, ic, gi, g1, m, tn, gn, lane);
+      issue_block(bufB, ic, gi, g1, m, tn, gn, lane);
+    }
+  };
+
+  if (qb < qe) {
+    if (wave == 0) load_static(m, ldc<amk_task_t>(m.tasks + qb), token, pos, L, ctl, lane);
+    else prefetch(qb);
   }
   __syncthreads();
 
-  const int qb = ldc<int32_t>(m.queue_start + blockIdx.x), qe = ldc<int32_t>(m.queue_start + blockIdx.x + 1);
   for (int idx = qb; idx < qe; ++idx) {
     const amk_task_t t = ldc<amk_task_t>(m.tasks + idx);
     const bool gemv = is_gemv(t.op);
     Gemv g = {0, 0, 1, 0, 0, 0};
     if (gemv) g = gemv_geom(m, t);
+    uint64_t* tr = m.trace ? m.trace + (size_t)idx * AMK_TRACE_FIELDS : nullptr;
 
-    // ---- phase 1: sync wave waits + loads the input; streaming waves prefetch weights
-    uint4 bufA[PIPE], bufB[PIPE];
-    Cursor ic;
-    int gi = 0, g0 = 0, g1 = 0;
+    // ---- B1a: the sync wave's counter wait
     if (wave == 0) {
-      const bool ok = wait_deps(m, t, m.tasks + idx, epoch, timeout_ticks, lane);
-      if (!ok) {
-        if (lane == 0) ctl.abort = 1;
-      } else {
-        switch (t.op) {
-          case AMK_OP_QKV:
-            if (t.layer == 0)
-              load_normed<true>(m.embed + (size_t)token * m.H, ldc<const uint16_t*>(&m.layers[0].attn_norm), m.H, m.eps, act, ctl, lane);
-            else
-              load_normed<false>(m.x + (size_t)(2 * t.layer) * m.H, ldc<const uint16_t*>(&m.layers[t.layer].attn_norm), m.H, m.eps, act,
-                                 ctl, lane);
-            break;
-          case AMK_OP_GATEUP:
-            load_normed<false>(m.x + (size_t)(2 * t.layer + 1) * m.H, ldc<const uint16_t*>(&m.layers[t.layer].mlp_norm), m.H, m.eps, act,
-                               ctl, lane);
-            break;
-          case AMK_OP_LMHEAD:
-            load_normed<false>(m.x + (size_t)(2 * m.L) * m.H, m.final_norm, m.H, m.eps, act, ctl, lane);
-            break;
-          case AMK_OP_O: load_plain(m.o + (size_t)t.layer * m.nq * m.hd, m.nq * m.hd, act, lane); break;
-          case AMK_OP_DOWN: load_plain(m.a + (size_t)t.layer * m.I, m.I, act, lane); break;
-          case AMK_OP_ATTN:
-            load_plain(m.q + (size_t)t.layer * m.nq * m.hd + (size_t)t.aux * m.group * m.hd, m.group * m.hd, act,
-                       lane);
-            break;
-          default: break;
-        }
-      }
-    } else if (gemv) {
-      const int sw = wave - 1;
-      g0 = wave_gbegin(g.G, sw);
-      g1 = wave_gbegin(g.G, sw + 1);
-      gi = g0;
-      if (g0 < g1) {
-        cursor_init(ic, m, t, g, g0);
-        issue_block(bufA, ic, gi, g1, m, t, g, lane);
-        issue_block(bufB, ic, gi, g1, m, t, g, lane);
-      }
+      if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_WAIT_BEGIN, (uint64_t)wall_clock64());
+      const bool ok = wait_deps(m, t, m.tasks + idx, epoch, timeout_ticks, lane, tr);
+      if (!ok && lane == 0) ctl.abort = 1;
+      if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_WAIT_END, (uint64_t)wall_clock64());
     }
-    __syncthreads();  // B1: input activation in LDS
+    __syncthreads();
     if (ctl.abort) return;
 
-    // ---- phase 2: compute
+    // ---- B1b: every wave moves its slice of the input activation
+    load_input(m, t, token, L, ctl, wave, lane);
+    __syncthreads();
+    if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());
+
+    // ---- compute
     if (gemv && wave != 0 && g0 < g1) {
       const int sw = wave - 1;
-      float* mypart = part + sw * pstride;
+      float* mypart = L.part + sw * pstride;
       int cj = g0 / g.gpr, cc = g0 - cj * g.gpr, cg = g0;
       float acc = 0.f;
       while (cg < g1) {
-        consume_block(bufA, cj, cc, cg, g1, acc, act, mypart, g, lane);
+        consume_block(bufA, cj, cc, cg, g1, acc, L.act, mypart, g, lane);
         issue_block(bufA, ic, gi, g1, m, t, g, lane);
-        consume_block(bufB, cj, cc, cg, g1, acc, act, mypart, g, lane);
+        consume_block(bufB, cj, cc, cg, g1, acc, L.act, mypart, g, lane);
         issue_block(bufB, ic, gi, g1, m, t, g, lane);
       }
       if (cc != 0) {
@@ -815,60 +935,67 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         if (lane == 0) mypart[cj] = s;
       }
     } else if (t.op == AMK_OP_ATTN) {
-      attention<GM, KB, EPL>(m, t, pos, kv, act, part, ctl, wave, lane);
+      attention<HD, GM>(m, t, pos, kv, L.act, L.part, ctl, wave, lane);
     }
     __syncthreads();  // B2: results in LDS
 
-    // ---- phase 3: sync wave publishes results, releases, signals
+    // ---- publish (sync wave), then stream the next task (streaming waves)
     if (wave == 0) {
+      if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_COMPUTE_END, (uint64_t)wall_clock64());
       switch (t.op) {
-        case AMK_OP_QKV: epi_qkv(m, t, g, part, pos, kv, ctl.rs, lane); break;
-        case AMK_OP_ATTN:
-          epi_attn<GM, KB, EPL>(m, t, part, ctl, pos, lane);
-          break;
-        case AMK_OP_COMBINE: combine(m, t, pos, lane); break;
-        case AMK_OP_O:
-          if (t.layer == 0) epi_o_layer0(m, t, g, part, token, lane);
-          else epi_rows(m, t, g, part, ctl.rs, logits, lane);
-          break;
-        case AMK_OP_GATEUP: case AMK_OP_DOWN: case AMK_OP_LMHEAD:
-          epi_rows(m, t, g, part, ctl.rs, logits, lane);
-          break;
+        case AMK_OP_QKV: epi_qkv(m, t, g, L, pos, kv, input_rs(m, ctl), lane); break;
+        case AMK_OP_ATTN: epi_attn<HD, GM>(m, t, L.part, ctl, pos, lane); break;
+        case AMK_OP_COMBINE: combine_heads(m, t.layer, t.begin, t.end, pos, lane); break;
+        case AMK_OP_O: case AMK_OP_DOWN: epi_residual(m, t, g, L, ctl, lane); break;
+        case AMK_OP_GATEUP: epi_gateup(m, t, g, L, input_rs(m, ctl), lane); break;
+        case AMK_OP_LMHEAD: epi_lmhead(m, t, g, L, input_rs(m, ctl), logits, lane); break;
         case AMK_OP_ARGMAX: argmax_final(m, t, lane); break;
         default: break;
       }
-      signal_done(m, t, lane);
+      if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_PUBLISHED, (uint64_t)wall_clock64());
+    }
+    __syncthreads();  // B3: result stores issued
+    if (wave == 0) {
+      release_signal(m, t.signal_counter, lane);
+      if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SIGNALLED, (uint64_t)wall_clock64());
+      if (idx + 1 < qe) load_static(m, ldc<amk_task_t>(m.tasks + idx + 1), token, pos, L, ctl, lane);
+    } else {
+      prefetch(idx + 1);
     }
   }
 }
 
 // ---------------------------------------------------------------- host side
-// Query groups up to 4 heads: 8 head dims per lane, 8 rows in flight per lane.
-// Groups of 5..8 heads: 4 head dims per lane, 4 rows in flight per lane.
-#define AMK_SMALL_GROUP 4, 8, 8
-#define AMK_LARGE_GROUP 8, 4, 4
+template <int HD, int GM>
+static const void* kernel_ptr() {
+  return (const void*)amk_decode_kernel<HD, GM>;
+}
 
-static const void* kernel_for(int group) {
-  return group <= 4 ? (const void*)amk_decode_kernel<AMK_SMALL_GROUP> : (const void*)amk_decode_kernel<AMK_LARGE_GROUP>;
+static const void* kernel_for(int head_dim, int group) {
+  const bool small = group <= 4;
+  if (head_dim == 64) return small ? kernel_ptr<64, 4>() : kernel_ptr<64, 8>();
+  return small ? kernel_ptr<128, 4>() : kernel_ptr<128, 8>();
 }
 
 extern "C" int amk_internal_threads(void) { return NT; }
 
-// Floats of LDS scratch the attention of one task needs (after the activation region).
+// Floats of LDS scratch the attention of one task needs (in the partials region).
 extern "C" int amk_internal_attn_scratch(int group, int head_dim) {
-  const int GM = group <= 4 ? 4 : 8, KB = group <= 4 ? 8 : 4, EPL = group <= 4 ? 8 : 4;
-  const int RP = NW * (64 / (head_dim / EPL));
-  return GM * RP * KB + NW * group * head_dim + group * head_dim;
+  const bool small = group <= 4;
+  if (head_dim == 64) return small ? AttnGeom<64, 4>::SCRATCH : AttnGeom<64, 8>::SCRATCH;
+  return small ? AttnGeom<128, 4>::SCRATCH : AttnGeom<128, 8>::SCRATCH;
 }
 
-extern "C" int amk_internal_prepare(int group, int lds_bytes) {
-  hipError_t e = hipFuncSetAttribute(kernel_for(group), hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+extern "C" int amk_internal_prepare(int head_dim, int group, int lds_bytes) {
+  hipError_t e =
+      hipFuncSetAttribute(kernel_for(head_dim, group), hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }
 
 // Largest number of co-resident workgroups of the kernel per CU for this LDS size.
-extern "C" int amk_internal_occupancy(int group, int lds_bytes, int* blocks_per_cu) {
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, kernel_for(group), NT, lds_bytes);
+extern "C" int amk_internal_occupancy(int head_dim, int group, int lds_bytes, int* blocks_per_cu) {
+  hipError_t e =
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, kernel_for(head_dim, group), NT, lds_bytes);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }
 
@@ -876,7 +1003,7 @@ extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos
                                    float* logits, uint64_t timeout_ticks, void* stream) {
   DevModel mm = *m;
   void* args[] = {&mm, &token, &pos, &epoch, &kv, &logits, &timeout_ticks};
-  hipError_t e = hipLaunchCooperativeKernel(kernel_for(m->group), dim3(m->n_cu), dim3(NT), args,
+  hipError_t e = hipLaunchCooperativeKernel(kernel_for(m->hd, m->group), dim3(m->n_cu), dim3(NT), args,
                                             (unsigned)m->lds_bytes, (hipStream_t)stream);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }

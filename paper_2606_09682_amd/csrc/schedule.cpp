@@ -12,8 +12,6 @@ namespace amk {
 
 namespace {
 
-bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
-
 void set_msg(std::string* why, const char* fmt, long a = 0, long b = 0) {
   if (!why) return;
   char buf[256];
@@ -52,8 +50,8 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
   }
   if (nq % nkv) { set_msg(why, "n_heads %ld not a multiple of n_kv_heads %ld", nq, nkv); return AMK_ERR_UNSUPPORTED; }
   if (nq / nkv > 8) { set_msg(why, "query group %ld > 8", nq / nkv); return AMK_ERR_UNSUPPORTED; }
-  if (!is_pow2(hd) || hd < 64 || hd > 256) {
-    set_msg(why, "head_dim %ld must be a power of two in [64, 256]", hd);
+  if (hd != 64 && hd != 128) {
+    set_msg(why, "head_dim %ld must be 64 or 128", hd);
     return AMK_ERR_UNSUPPORTED;
   }
   // every weight row must be a whole number of 16-byte vectors in both formats

@@ -57,7 +57,9 @@ int main(void) {
   E(AMK_OP_QKV) E(AMK_OP_ATTN) E(AMK_OP_COMBINE) E(AMK_OP_O) E(AMK_OP_GATEUP) E(AMK_OP_DOWN) E(AMK_OP_LMHEAD)
   E(AMK_OP_ARGMAX) E(AMK_CHECK_OK) E(AMK_CHECK_WELL_FORMED) E(AMK_CHECK_CAPACITY) E(AMK_CHECK_WAIT_SATISFIABLE)
   E(AMK_CHECK_ALL_JOIN) E(AMK_CHECK_ACYCLIC) E(AMK_CHECK_QUEUE_ORDER) E(AMK_CHECK_RACE) E(AMK_CHECK_KV_ORDER)
-  E(AMK_CHECK_OUTPUT)
+  E(AMK_CHECK_OUTPUT) E(AMK_TRACE_FIELDS) E(AMK_TRACE_WAIT_BEGIN) E(AMK_TRACE_WAIT_END) E(AMK_TRACE_INPUT_READY)
+  E(AMK_TRACE_COMPUTE_END) E(AMK_TRACE_SIGNALLED) E(AMK_TRACE_PUBLISHED)
+  E(AMK_TRACE_RELEASED) E(AMK_TRACE_SATISFIED)
   return 0;
 }
 '''
