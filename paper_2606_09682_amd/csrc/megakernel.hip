@@ -19,12 +19,15 @@
 //   B1a  the sync wave's counter wait is satisfied (or the launch aborts)
 //   B1b  the input activation is in LDS
 //   B2   the task's compute is done (partials / attention output in LDS)
-//   B3   the sync wave has issued the task's result stores
+//   B3   the sync wave has stored, released and signalled the task's results
 // The streaming waves issue the weight loads of their NEXT task right after
 // B3.  Memory requests of one CU are served roughly in order, so loads issued
-// before the result stores would delay the release and hence every consumer
-// on other CUs; issued after them, the loads stream while the counters
-// propagate and the next input is fetched.
+// before the result stores, the release or the counter increment would delay
+// every consumer on other CUs; issued after them, the loads stream while the
+// counters propagate and the next input is fetched.  The pipeline is kept
+// shallow (two halves of PIPE granules per wave): measured on the
+// Llama-3-8B shape, deeper pipelines both delay the sync wave's polls and
+// input loads and stream no faster.
 //
 // Only the sync wave executes agent-scope acquire/release sequences: their
 // vmcnt(0) drains would otherwise stall the streaming waves' in-flight loads.
@@ -43,7 +46,7 @@ namespace amk {
 constexpr int NT = 512;       // threads per workgroup
 constexpr int NW = NT / 64;   // waves
 constexpr int NSW = NW - 1;   // streaming waves
-constexpr int PIPE = 8;       // 1-KiB granules per pipeline half, per wave
+constexpr int PIPE = 4;       // 1-KiB granules per pipeline half, per wave
 constexpr int GRAN = 1024;    // bytes per wave-wide 16-B-per-lane load
 
 struct Ctl {
@@ -953,11 +956,11 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         default: break;
       }
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_PUBLISHED, (uint64_t)wall_clock64());
-    }
-    __syncthreads();  // B3: result stores issued
-    if (wave == 0) {
       release_signal(m, t.signal_counter, lane);
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SIGNALLED, (uint64_t)wall_clock64());
+    }
+    __syncthreads();  // B3: results released and signalled
+    if (wave == 0) {
       if (idx + 1 < qe) load_static(m, ldc<amk_task_t>(m.tasks + idx + 1), token, pos, L, ctl, lane);
     } else {
       prefetch(idx + 1);
