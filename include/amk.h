@@ -197,7 +197,7 @@ int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_t
 enum {
   AMK_OP_QKV = 1,      /* RMSNorm + q/k/v GEMV of RoPE row-pair units [begin, end) + RoPE + KV append */
   AMK_OP_ATTN = 2,     /* partial attention of KV head `aux`, position split `begin` of `end` */
-  AMK_OP_COMBINE = 3,  /* merge the position splits of query heads [begin, end) */
+  AMK_OP_COMBINE = 3,  /* merge the position splits of query heads [begin, end) (inline, see below) */
   AMK_OP_O = 4,        /* rows [begin, end) of x1 = x + Wo o */
   AMK_OP_GATEUP = 5,   /* rows [begin, end) of a = silu(Wg h2) * (Wu h2), h2 = RMSNorm(x1) */
   AMK_OP_DOWN = 6,     /* rows [begin, end) of x2 = x1 + Wd a */
@@ -206,22 +206,30 @@ enum {
 };
 
 #define AMK_MAX_WAITS 4
+/* Queue value of an inline task: it runs on no queue of its own but at the
+ * end of whichever producer of its single wait counter increments that
+ * counter last (that producer's chain_counter names the inline task's
+ * signal counter).  Used for the COMBINE of a KV group's attention splits. */
+#define AMK_CU_INLINE (-1)
 
 /* Fixed-size task descriptor (64 bytes), the unit the device walks.  A task
  * waits until, for every i < n_wait, counter wait_counter[i] has been
  * incremented wait_count[i] times in this launch, then runs, then increments
- * signal_counter (if >= 0) once. */
+ * signal_counter (if >= 0) once.  If chain_counter >= 0 and this task's
+ * increment of signal_counter is the last of the launch, it then runs the
+ * inline task waiting on signal_counter, which increments chain_counter. */
 typedef struct {
   uint16_t op;
   uint16_t layer;
-  int32_t cu;          /* queue (workgroup index) that runs the task */
-  int32_t seq;         /* position inside that queue, 0-based, contiguous */
+  int32_t cu;          /* queue (workgroup index) that runs the task, or AMK_CU_INLINE */
+  int32_t seq;         /* position inside that queue, 0-based, contiguous (0 for inline tasks) */
   int32_t begin, end;  /* op-specific range, see AMK_OP_* */
-  int32_t aux;         /* op-specific */
-  int32_t n_wait;
+  int16_t aux;         /* op-specific */
+  int16_t n_wait;
   int32_t wait_counter[AMK_MAX_WAITS];
   int32_t wait_count[AMK_MAX_WAITS];
   int32_t signal_counter;
+  int32_t chain_counter;
 } amk_task_t;
 
 typedef struct {
@@ -243,7 +251,8 @@ enum {
   AMK_CHECK_QUEUE_ORDER = 6,   /* a consumer queued before its producer on the same CU */
   AMK_CHECK_RACE = 7,          /* a read not ordered after every writer of the region it reads */
   AMK_CHECK_KV_ORDER = 8,      /* a KV-cache read not ordered after this pass's append */
-  AMK_CHECK_OUTPUT = 9         /* an output region written twice or never */
+  AMK_CHECK_OUTPUT = 9,        /* an output region written twice or never */
+  AMK_CHECK_INLINE = 10        /* an inline task or a chain counter that does not pair up */
 };
 
 /* Number of tasks / counters the schedule of cfg has on n_cu queues (after

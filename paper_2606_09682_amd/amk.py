@@ -31,12 +31,14 @@ AMK_WEIGHTS_W8A16 = 1
 
 AMK_OP_QKV, AMK_OP_ATTN, AMK_OP_COMBINE, AMK_OP_O, AMK_OP_GATEUP, AMK_OP_DOWN, AMK_OP_LMHEAD, AMK_OP_ARGMAX = range(1, 9)
 AMK_MAX_WAITS = 4
+AMK_CU_INLINE = -1
 AMK_TRACE_FIELDS = 8
 (AMK_TRACE_WAIT_BEGIN, AMK_TRACE_WAIT_END, AMK_TRACE_INPUT_READY, AMK_TRACE_COMPUTE_END,
  AMK_TRACE_SIGNALLED, AMK_TRACE_PUBLISHED, AMK_TRACE_RELEASED, AMK_TRACE_SATISFIED) = range(8)
 
 (AMK_CHECK_OK, AMK_CHECK_WELL_FORMED, AMK_CHECK_CAPACITY, AMK_CHECK_WAIT_SATISFIABLE, AMK_CHECK_ALL_JOIN,
- AMK_CHECK_ACYCLIC, AMK_CHECK_QUEUE_ORDER, AMK_CHECK_RACE, AMK_CHECK_KV_ORDER, AMK_CHECK_OUTPUT) = range(10)
+ AMK_CHECK_ACYCLIC, AMK_CHECK_QUEUE_ORDER, AMK_CHECK_RACE, AMK_CHECK_KV_ORDER, AMK_CHECK_OUTPUT,
+ AMK_CHECK_INLINE) = range(11)
 
 
 # ---- structures ---------------------------------------------------------------
@@ -69,9 +71,10 @@ class amk_tuning_t(ctypes.Structure):
 
 class amk_task_t(ctypes.Structure):
     _fields_ = [("op", ctypes.c_uint16), ("layer", ctypes.c_uint16), ("cu", ctypes.c_int32), ("seq", ctypes.c_int32),
-                ("begin", ctypes.c_int32), ("end", ctypes.c_int32), ("aux", ctypes.c_int32),
-                ("n_wait", ctypes.c_int32), ("wait_counter", ctypes.c_int32 * AMK_MAX_WAITS),
-                ("wait_count", ctypes.c_int32 * AMK_MAX_WAITS), ("signal_counter", ctypes.c_int32)]
+                ("begin", ctypes.c_int32), ("end", ctypes.c_int32), ("aux", ctypes.c_int16),
+                ("n_wait", ctypes.c_int16), ("wait_counter", ctypes.c_int32 * AMK_MAX_WAITS),
+                ("wait_count", ctypes.c_int32 * AMK_MAX_WAITS), ("signal_counter", ctypes.c_int32),
+                ("chain_counter", ctypes.c_int32)]
 
 
 class amk_check_report_t(ctypes.Structure):

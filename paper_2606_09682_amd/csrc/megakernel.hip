@@ -368,6 +368,19 @@ __device__ __forceinline__ void release_signal(const DevModel& m, int counter, i
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Release, increment `counter`, and report whether this increment brought it
+// to `target` (the last producer of this launch).  The caller that gets true
+// acquires before reading what the other producers released.
+__device__ __forceinline__ bool release_signal_last(const DevModel& m, int counter, uint32_t target, int lane) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  uint32_t old = 0;
+  if (lane == 0)
+    old = __hip_atomic_fetch_add(m.counters + (size_t)counter * kCounterStride, 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+  old = (uint32_t)__builtin_amdgcn_readfirstlane((int)old);
+  return (int32_t)(old + 1u - target) == 0;
+}
+
 // ---------------------------------------------------------------- static per-task data
 // Data that does not depend on this launch's results (norm gains, RoPE
 // factors, int8 row scales, the layer-0 embedding rows) is fetched before
@@ -826,15 +839,34 @@ __device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t
   }
 }
 
+// Number of position splits with work at `pos` (split s covers positions
+// [s * chunk, (s + 1) * chunk) of 0..pos).
+__device__ __forceinline__ int active_splits(const DevModel& m, int pos, int* chunk_out) {
+  const int n_pos = pos + 1;
+  const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
+  if (chunk_out) *chunk_out = chunk;
+  return (n_pos + chunk - 1) / chunk;
+}
+
+// Store this split's result: the normalised head outputs when it is the only
+// split with work, else the (m, l, unnormalised acc) record the combine reads.
 template <int HD, int GM>
 __device__ __forceinline__ void epi_attn(const DevModel& m, const amk_task_t& t, const float* scr, const Ctl& ctl,
                                          int pos, int lane) {
   using A = AttnGeom<HD, GM>;
   const int G = m.group;
-  const int n_pos = pos + 1;
-  const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
-  if (t.begin * chunk >= n_pos) return;  // empty split: the combine ignores it
+  int chunk;
+  const int active = active_splits(m, pos, &chunk);
+  if (t.begin >= active) return;  // empty split: nothing to publish
   const float* out = scr + GM * A::SC + NW * GM * HD;
+  if (active == 1) {
+    float* o = m.o + (size_t)t.layer * m.nq * HD + (size_t)t.aux * G * HD;
+    for (int h = 0; h < G; ++h) {
+      const float inv = 1.0f / ctl.l_run[h];
+      for (int e = lane; e < HD; e += 64) stg<float>(o + h * HD + e, out[h * HD + e] * inv);
+    }
+    return;
+  }
   const int rec = G * (kPartHead + HD);
   float* dst = m.part + ((size_t)(t.layer * m.nkv + t.aux) * m.nsplit + t.begin) * rec;
   for (int h = 0; h < G; ++h) {
@@ -916,8 +948,11 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     __syncthreads();
     if (ctl.abort) return;
 
+    // an attention split with no positions at `pos` has no input and no work
+    const bool idle = t.op == AMK_OP_ATTN && t.begin >= active_splits(m, pos, nullptr);
+
     // ---- B1b: every wave moves its slice of the input activation
-    load_input(m, t, token, L, ctl, wave, lane);
+    if (!idle) load_input(m, t, token, L, ctl, wave, lane);
     __syncthreads();
     if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());
 
@@ -937,7 +972,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         const float s = wave_sum(acc);
         if (lane == 0) mypart[cj] = s;
       }
-    } else if (t.op == AMK_OP_ATTN) {
+    } else if (t.op == AMK_OP_ATTN && !idle) {
       attention<HD, GM>(m, t, pos, kv, L.act, L.part, ctl, wave, lane);
     }
     __syncthreads();  // B2: results in LDS
@@ -956,7 +991,18 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         default: break;
       }
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_PUBLISHED, (uint64_t)wall_clock64());
-      release_signal(m, t.signal_counter, lane);
+      if (t.chain_counter >= 0) {
+        // attention split: the last split of this KV head to finish runs the
+        // head's inline combine (its producers are the head's nsplit splits)
+        if (release_signal_last(m, t.signal_counter, epoch * (uint32_t)m.nsplit, lane)) {
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          if (active_splits(m, pos, nullptr) > 1)
+            combine_heads(m, t.layer, t.aux * m.group, (t.aux + 1) * m.group, pos, lane);
+          release_signal(m, t.chain_counter, lane);
+        }
+      } else {
+        release_signal(m, t.signal_counter, lane);
+      }
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SIGNALLED, (uint64_t)wall_clock64());
     }
     __syncthreads();  // B3: results released and signalled

@@ -99,12 +99,14 @@ Schedule build_schedule(const Shape& s, int n_cu) {
   int rot = 0;  // rotating start CU for stages narrower than the grid
 
   auto add = [&](int op, int layer, int cu, int b, int e, int aux,
-                 std::vector<std::pair<int, int>> waits, int sig) {
+                 std::vector<std::pair<int, int>> waits, int sig, int chain = -1) {
     amk_task_t t;
     std::memset(&t, 0, sizeof(t));
-    t.op = (uint16_t)op; t.layer = (uint16_t)layer; t.cu = cu; t.seq = qlen[cu]++;
-    t.begin = b; t.end = e; t.aux = aux;
-    t.n_wait = (int)waits.size();
+    t.op = (uint16_t)op; t.layer = (uint16_t)layer; t.cu = cu;
+    t.seq = cu == AMK_CU_INLINE ? 0 : qlen[cu]++;
+    t.begin = b; t.end = e; t.aux = (int16_t)aux;
+    t.n_wait = (int16_t)waits.size();
+    t.chain_counter = chain;
     for (int i = 0; i < AMK_MAX_WAITS; ++i) { t.wait_counter[i] = -1; t.wait_count[i] = 0; }
     for (size_t i = 0; i < waits.size(); ++i) {
       t.wait_counter[i] = waits[i].first; t.wait_count[i] = waits[i].second;
@@ -140,16 +142,22 @@ Schedule build_schedule(const Shape& s, int n_cu) {
   int prev_c = -1, prev_n = 0;  // counter of the stage producing the layer input
   for (int l = 0; l < s.L; ++l) {
     auto qkv = stage(AMK_OP_QKV, l, s.units, 2, prev_c, prev_n);
-    // attention: one task per (KV head, position split)
-    const int c_attn = n_ctr++;
+    // attention: one task per (KV head, position split).  The splits of a KV
+    // head signal that head's counter; the split that increments it last
+    // runs the head's inline COMBINE, which signals c_done.
+    const int c_done = n_ctr++;
+    const int c_grp0 = n_ctr;
+    n_ctr += s.nkv;
     const int n_attn = s.nkv * s.nsplit;
     for (int i = 0; i < n_attn; ++i) {
-      add(AMK_OP_ATTN, l, cu_of(i, n_attn), i % s.nsplit, s.nsplit, i / s.nsplit,
-          {{qkv.first, qkv.second}}, c_attn);
+      const int g = i / s.nsplit;
+      add(AMK_OP_ATTN, l, cu_of(i, n_attn), i % s.nsplit, s.nsplit, g, {{qkv.first, qkv.second}}, c_grp0 + g,
+          c_done);
     }
     bump(n_attn);
-    auto comb = stage(AMK_OP_COMBINE, l, s.nq, 0, c_attn, n_attn);
-    auto o = stage(AMK_OP_O, l, s.H, 1, comb.first, comb.second);
+    for (int g = 0; g < s.nkv; ++g)
+      add(AMK_OP_COMBINE, l, AMK_CU_INLINE, g * s.group, (g + 1) * s.group, g, {{c_grp0 + g, s.nsplit}}, c_done);
+    auto o = stage(AMK_OP_O, l, s.H, 1, c_done, s.nkv);
     auto gu = stage(AMK_OP_GATEUP, l, s.I, 2, o.first, o.second);
     auto dn = stage(AMK_OP_DOWN, l, s.H, 1, gu.first, gu.second);
     prev_c = dn.first; prev_n = dn.second;
@@ -170,11 +178,14 @@ Schedule build_schedule(const Shape& s, int n_cu) {
 }
 
 void finalize_queues(std::vector<amk_task_t>* tasks, int n_cu, std::vector<int32_t>* queue_start) {
-  std::stable_sort(tasks->begin(), tasks->end(), [](const amk_task_t& a, const amk_task_t& b) {
-    return a.cu != b.cu ? a.cu < b.cu : a.seq < b.seq;
+  // queued tasks by (cu, seq); inline tasks (no queue) after all of them
+  auto key = [n_cu](const amk_task_t& t) { return t.cu == AMK_CU_INLINE ? n_cu : t.cu; };
+  std::stable_sort(tasks->begin(), tasks->end(), [&](const amk_task_t& a, const amk_task_t& b) {
+    return key(a) != key(b) ? key(a) < key(b) : a.seq < b.seq;
   });
   queue_start->assign(n_cu + 1, 0);
-  for (const auto& t : *tasks) (*queue_start)[t.cu + 1]++;
+  for (const auto& t : *tasks)
+    if (t.cu != AMK_CU_INLINE) (*queue_start)[t.cu + 1]++;
   for (int c = 0; c < n_cu; ++c) (*queue_start)[c + 1] += (*queue_start)[c];
 }
 
@@ -297,8 +308,13 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     const amk_task_t& t = tasks[i];
     if (t.op < AMK_OP_QKV || t.op > AMK_OP_ARGMAX)
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: unknown op %ld", i, t.op);
-    if (t.cu < 0 || t.cu >= n_cu)
+    const bool inl = t.cu == AMK_CU_INLINE;
+    if (!inl && (t.cu < 0 || t.cu >= n_cu))
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: queue %ld out of range", i, t.cu);
+    if (inl && (t.op != AMK_OP_COMBINE || t.seq != 0))
+      return R.fail(AMK_CHECK_INLINE, i, -1, "task %ld: only a COMBINE (seq 0) may run inline", i);
+    if (t.chain_counter < -1 || t.chain_counter >= n_counters)
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: chain counter %ld out of range", i, t.chain_counter);
     const bool layered = t.op <= AMK_OP_DOWN;
     if (layered && t.layer >= s.L)
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: layer %ld out of range", i, t.layer);
@@ -335,7 +351,7 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
       return R.fail(AMK_CHECK_CAPACITY, i, -1, "task %ld: %ld rows exceed the per-task cap", i, task_jobs(s, t));
     if (t.op == AMK_OP_COMBINE && t.end - t.begin > 64)
       return R.fail(AMK_CHECK_CAPACITY, i, -1, "task %ld: combine of more than 64 heads", i);
-    qlen[t.cu]++;
+    if (!inl) qlen[t.cu]++;
   }
   // queue positions must be 0..len-1, each exactly once
   {
@@ -343,6 +359,7 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     for (int c = 0; c < n_cu; ++c) at[c].assign(qlen[c], -1);
     for (int i = 0; i < n; ++i) {
       const amk_task_t& t = tasks[i];
+      if (t.cu == AMK_CU_INLINE) continue;
       if (t.seq < 0 || t.seq >= qlen[t.cu] || at[t.cu][t.seq] != -1)
         return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: queue position %ld invalid or repeated", i, t.seq);
       at[t.cu][t.seq] = i;
@@ -369,6 +386,32 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     }
   }
 
+  // ---- 2b. inline tasks: one wait; every producer of that counter chains to
+  //          the inline task's signal; every chaining task feeds exactly one
+  //          inline task ------------------------------------------------------
+  std::vector<int> inline_of(n_counters, -1);  // counter -> inline task waiting on it
+  for (int i = 0; i < n; ++i) {
+    const amk_task_t& t = tasks[i];
+    if (t.cu != AMK_CU_INLINE) continue;
+    if (t.n_wait != 1 || t.signal_counter < 0)
+      return R.fail(AMK_CHECK_INLINE, i, -1, "inline task %ld needs exactly one wait and a signal", i);
+    const int c = t.wait_counter[0];
+    if (inline_of[c] != -1)
+      return R.fail(AMK_CHECK_INLINE, i, inline_of[c], "counter %ld feeds two inline tasks", c);
+    inline_of[c] = i;
+    for (int p : producers[c])
+      if (tasks[p].chain_counter != t.signal_counter || tasks[p].cu == AMK_CU_INLINE)
+        return R.fail(AMK_CHECK_INLINE, i, p, "producer %ld of inline task %ld does not chain to its signal", p, i);
+  }
+  for (int i = 0; i < n; ++i) {
+    const amk_task_t& t = tasks[i];
+    if (t.chain_counter < 0) continue;
+    const int k = t.signal_counter >= 0 ? inline_of[t.signal_counter] : -1;
+    if (k < 0 || tasks[k].signal_counter != t.chain_counter)
+      return R.fail(AMK_CHECK_INLINE, i, k, "task %ld chains to counter %ld without a matching inline task", i,
+                    t.chain_counter);
+  }
+
   // ---- 3. queue order: a producer on the same CU must be queued earlier ------
   long n_edges = 0;
   for (int i = 0; i < n; ++i) {
@@ -376,7 +419,7 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     for (int w = 0; w < t.n_wait; ++w) {
       for (int p : producers[t.wait_counter[w]]) {
         ++n_edges;
-        if (tasks[p].cu == t.cu && tasks[p].seq >= t.seq)
+        if (t.cu != AMK_CU_INLINE && tasks[p].cu == t.cu && tasks[p].seq >= t.seq)
           return R.fail(AMK_CHECK_QUEUE_ORDER, i, p, "task %ld on queue %ld waits on task %ld queued at or after it", i,
                         t.cu, p);
       }
@@ -390,10 +433,12 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
   // global order for the happens-before pass below.
   std::vector<std::vector<int>> queue(n_cu);
   for (int c = 0; c < n_cu; ++c) queue[c].assign(qlen[c], -1);
-  for (int i = 0; i < n; ++i) queue[tasks[i].cu][tasks[i].seq] = i;
+  for (int i = 0; i < n; ++i)
+    if (tasks[i].cu != AMK_CU_INLINE) queue[tasks[i].cu][tasks[i].seq] = i;
   std::vector<int> indeg(n, 0), remaining(n_counters);
   for (int c = 0; c < n_counters; ++c) remaining[c] = (int)producers[c].size();
-  for (int i = 0; i < n; ++i) indeg[i] = (tasks[i].seq > 0 ? 1 : 0) + tasks[i].n_wait;
+  for (int i = 0; i < n; ++i)
+    indeg[i] = (tasks[i].cu != AMK_CU_INLINE && tasks[i].seq > 0 ? 1 : 0) + tasks[i].n_wait;
   std::vector<int> order;
   order.reserve(n);
   std::vector<int> stack;
@@ -404,7 +449,7 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     stack.pop_back();
     order.push_back(i);
     const amk_task_t& t = tasks[i];
-    if (t.seq + 1 < qlen[t.cu]) {
+    if (t.cu != AMK_CU_INLINE && t.seq + 1 < qlen[t.cu]) {
       const int nx = queue[t.cu][t.seq + 1];
       if (--indeg[nx] == 0) stack.push_back(nx);
     }
@@ -426,7 +471,7 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
       seen[cur] = step++;
       const amk_task_t& t = tasks[cur];
       int nxt = -1;
-      if (t.seq > 0 && !done[queue[t.cu][t.seq - 1]]) nxt = queue[t.cu][t.seq - 1];
+      if (t.cu != AMK_CU_INLINE && t.seq > 0 && !done[queue[t.cu][t.seq - 1]]) nxt = queue[t.cu][t.seq - 1];
       for (int w = 0; nxt < 0 && w < t.n_wait; ++w)
         for (int p : producers[t.wait_counter[w]])
           if (!done[p]) { nxt = p; break; }
@@ -479,38 +524,44 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
       return R.fail(AMK_CHECK_OUTPUT, -1, -1, "buffer %ld written up to %ld only", b, at);
   }
 
-  // vector clocks: vc[c] = highest queue position on CU c that happened before
-  std::vector<int32_t> q_vc((size_t)n_cu * n_cu, -1);        // clock of each queue's last task
-  std::vector<int32_t> ctr_vc((size_t)n_counters * n_cu, -1);// join of each counter's producers
-  std::vector<int> ctr_left(n_counters);
-  for (int c = 0; c < n_counters; ++c) ctr_left[c] = (int)producers[c].size();
-  std::vector<int32_t> vc(n_cu);
+  // vector clocks: vc[c] = highest queue position on queue c that happened
+  // before; each inline task gets a virtual queue n_cu + k of its own
+  std::vector<int> vq(n, -1);
+  int n_inline = 0;
+  for (int i = 0; i < n; ++i)
+    if (tasks[i].cu == AMK_CU_INLINE) vq[i] = n_cu + n_inline++;
+  const int W = n_cu + n_inline;
+  auto qof = [&](int i) { return tasks[i].cu == AMK_CU_INLINE ? vq[i] : tasks[i].cu; };
+  std::vector<int32_t> q_vc((size_t)n_cu * W, -1);          // clock of each queue's last task
+  std::vector<int32_t> ctr_vc((size_t)n_counters * W, -1);  // join of each counter's producers
+  std::vector<int32_t> vc(W);
   for (int i : order) {
     const amk_task_t& t = tasks[i];
-    std::copy(q_vc.begin() + (size_t)t.cu * n_cu, q_vc.begin() + (size_t)(t.cu + 1) * n_cu, vc.begin());
+    if (t.cu == AMK_CU_INLINE) std::fill(vc.begin(), vc.end(), -1);
+    else std::copy(q_vc.begin() + (size_t)t.cu * W, q_vc.begin() + (size_t)(t.cu + 1) * W, vc.begin());
     for (int w = 0; w < t.n_wait; ++w) {
-      const int32_t* cv = &ctr_vc[(size_t)t.wait_counter[w] * n_cu];
-      for (int c = 0; c < n_cu; ++c) vc[c] = std::max(vc[c], cv[c]);
+      const int32_t* cv = &ctr_vc[(size_t)t.wait_counter[w] * W];
+      for (int c = 0; c < W; ++c) vc[c] = std::max(vc[c], cv[c]);
     }
-    vc[t.cu] = t.seq;
+    vc[qof(i)] = t.seq;
     // reads
     accesses(s, ids, t, &rd, &wr);
     for (auto& a : rd) {
       for (auto& w : writers[a.buf]) {
         if (w.hi <= a.lo || w.lo >= a.hi) continue;
-        const amk_task_t& wt = tasks[w.task];
         if (w.task == i) continue;
-        if (vc[wt.cu] < wt.seq) {
+        const amk_task_t& wt = tasks[w.task];
+        if (vc[qof(w.task)] < wt.seq) {
           const int rule = ids.is_kv(a.buf) ? AMK_CHECK_KV_ORDER : AMK_CHECK_RACE;
           return R.fail(rule, i, w.task, "task %ld reads buffer %ld before writer task %ld is ordered", i, a.buf,
                         w.task);
         }
       }
     }
-    std::copy(vc.begin(), vc.end(), q_vc.begin() + (size_t)t.cu * n_cu);
+    if (t.cu != AMK_CU_INLINE) std::copy(vc.begin(), vc.end(), q_vc.begin() + (size_t)t.cu * W);
     if (t.signal_counter >= 0) {
-      int32_t* cv = &ctr_vc[(size_t)t.signal_counter * n_cu];
-      for (int c = 0; c < n_cu; ++c) cv[c] = std::max(cv[c], vc[c]);
+      int32_t* cv = &ctr_vc[(size_t)t.signal_counter * W];
+      for (int c = 0; c < W; ++c) cv[c] = std::max(cv[c], vc[c]);
     }
   }
   return true;

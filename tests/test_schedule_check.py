@@ -64,9 +64,12 @@ def test_real_lowering_accepted(lib, name, n_cu):
     tasks, nc = amk.amk_schedule_export(cfg, n_cu)
     rep = check(cfg, tasks, nc, n_cu)
     assert rep.ok == 1, rep.message
-    # one queue per CU, every queue used, seq contiguous
+    # one queue per CU, every queue used, seq contiguous; inline tasks sit on no queue
     seen = {}
     for t in tasks:
+        if t.cu == amk.AMK_CU_INLINE:
+            assert t.op == amk.AMK_OP_COMBINE
+            continue
         seen.setdefault(t.cu, []).append(t.seq)
     assert sorted(seen) == list(range(n_cu))
     for c, seqs in seen.items():
@@ -85,6 +88,10 @@ def test_schedule_shape_8b(lib):
     assert ops.count(amk.AMK_OP_DOWN) == 256 * L
     assert ops.count(amk.AMK_OP_LMHEAD) == 256
     assert ops.count(amk.AMK_OP_ARGMAX) == 1
+    # one inline combine per (layer, KV head), fed by that head's 32 splits
+    comb = [t for t in tasks if t.op == amk.AMK_OP_COMBINE]
+    assert len(comb) == 8 * L and all(t.cu == amk.AMK_CU_INLINE for t in comb)
+    assert all(t.wait_count[0] == 32 for t in comb)
     # every QKV task owns whole RoPE row pairs: 48 heads * 64 pairs / 256 = 12 units each
     assert {t.end - t.begin for t in tasks if t.op == amk.AMK_OP_QKV} == {12}
 
@@ -245,3 +252,57 @@ def test_random_single_mutations_never_crash(tiny_sched):
         setattr(m[i], f, getattr(m[i], f) + rng.choice([-3, -1, 1, 2, 1000]))
         rep = check(cfg, m, nc)
         assert rep.ok in (0, 1)
+
+
+# ------------------------------------------------------------------ inline combine
+def test_inline_task_with_two_waits_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_COMBINE, 1)
+    t = m[i]
+    t.wait_counter[1] = t.wait_counter[0]
+    t.wait_count[1] = t.wait_count[0]
+    t.n_wait = 2
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_INLINE, rep.message
+
+
+def test_chain_to_wrong_counter_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_ATTN, 0, lambda t: t.begin == 3)
+    m[i].chain_counter = m[find(m, amk.AMK_OP_O, 0)].signal_counter
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_INLINE, rep.message
+
+
+def test_split_without_chain_rejected(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_ATTN, 2, lambda t: t.begin == 5)
+    m[i].chain_counter = -1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_INLINE, rep.message
+
+
+def test_inline_task_only_for_combine(tiny_sched):
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_ARGMAX)
+    m[i].cu = amk.AMK_CU_INLINE
+    m[i].seq = 0
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule in (amk.AMK_CHECK_INLINE, amk.AMK_CHECK_WELL_FORMED), rep.message
+
+
+def test_o_reading_before_combine_rejected(tiny_sched):
+    """O waiting on the attention splits' head counter instead of the combine
+    output: it would read the attention output before the combine wrote it."""
+    cfg, tasks, nc = tiny_sched
+    m = clone(tasks)
+    comb = find(m, amk.AMK_OP_COMBINE, 1)
+    i = find(m, amk.AMK_OP_O, 1)
+    m[i].wait_counter[0] = m[comb].wait_counter[0]
+    m[i].wait_count[0] = m[comb].wait_count[0]
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule in (amk.AMK_CHECK_RACE, amk.AMK_CHECK_INLINE), rep.message
