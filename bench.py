@@ -134,6 +134,8 @@ def main():
     ap.add_argument("--config", default="llama3_8b")
     ap.add_argument("--variants", default="all", help="'all' or 'main' (bf16 at position 0 only)")
     ap.add_argument("--no-check", action="store_true", help="skip the oracle gate (profiling runs)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported by this build "
@@ -141,6 +143,18 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_probe:
+        # a plain copy kernel of known traffic: reads and writes BYTES once per launch
+        torch.cuda.set_device(0)
+        n = args.copy_probe // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": args.copy_probe, "launches": 3}), flush=True)
+        return
 
     import synth
     from paper_2606_09682_amd import amk

@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define AMK_ABI_VERSION 1
+#define AMK_ABI_VERSION 2
 
 /* ---- status codes ------------------------------------------------------ */
 enum {
@@ -108,6 +108,8 @@ typedef struct {
   int32_t timeout_us;       /* deadline of one device counter wait in microseconds; 0 = 2 s */
   int32_t max_rows_per_task;/* cap on rows of one GEMV task; 0 = 1024 */
   int32_t trace;            /* 1: record per-task timestamps (see amk_trace_copy) */
+  int32_t short_context;    /* steps with pos + 1 <= short_context run the short-context schedule
+                               (AMK_SCHEDULE_SHORT); 0 = 256; negative = never */
 } amk_tuning_t;
 
 typedef struct amk_handle_s* amk_handle_t;
@@ -120,6 +122,8 @@ typedef struct amk_handle_s* amk_handle_t;
  * the schedule tables, counters, scratch activations and the RoPE table.
  * Weight pointers are BORROWED: they must stay valid and unchanged until
  * amk_destroy(); nothing is copied or repacked.  tuning may be NULL.
+ * Both schedule variants (AMK_SCHEDULE_SHORT / _LONG) are built and checked;
+ * each step runs the one its position selects (amk_tuning_t.short_context).
  * On failure *out is set to NULL and nothing stays allocated. */
 int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
                amk_handle_t* out);
@@ -180,23 +184,38 @@ enum {
   AMK_TRACE_COMPUTE_END = 3,/* every wave finished the task's compute */
   AMK_TRACE_SIGNALLED = 4,  /* results published, counter incremented */
   AMK_TRACE_PUBLISHED = 5,  /* result stores issued, before the release fence */
-  AMK_TRACE_RELEASED = 6,   /* release fence done, before the counter increment */
+  AMK_TRACE_CHAINED = 6,    /* inline task run by this task finished and signalled (0: none ran) */
   AMK_TRACE_SATISFIED = 7   /* counters observed satisfied, before the acquire fence */
 };
 
 /* Copy the per-task timestamps of the last finished step of a handle created
  * with tuning.trace = 1 into dst[capacity] (host memory), AMK_TRACE_FIELDS
- * uint64 per task, tasks in amk_schedule_export() order.  Timestamps are the
- * device's constant 100 MHz wall clock.  Synchronises the handle's stream.
- * *n_tasks receives the task count.  AMK_ERR_BAD_STATE if tracing is off. */
-int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks);
+ * uint64 per task, tasks in amk_schedule_export() order of the schedule
+ * variant that step ran (*variant, may be NULL).  Timestamps are the device's
+ * constant 100 MHz wall clock.  Synchronises the handle's stream.  *n_tasks
+ * receives the task count.  AMK_ERR_BAD_STATE if tracing is off or nothing
+ * was launched. */
+int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks, int32_t* variant);
 
 /* ---- schedule introspection (CPU only, no device needed) -------------------- */
 
-/* Operations of the task graph, in the order of one layer. */
+/* Schedule variants.  Both compute the same step; they differ in where the
+ * attention runs.  SHORT: the last QKV task of each KV group to finish runs
+ * that group's whole attention inline (no attention stage).  LONG: the
+ * attention of each KV group is split over `attn_splits` position ranges on
+ * as many queues (flash-decoding style), and the last split of a group to
+ * finish merges the splits inline. */
+enum { AMK_SCHEDULE_SHORT = 0, AMK_SCHEDULE_LONG = 1 };
+
+/* Operations of the task graph, in the order of one layer.
+ * QKV units: unit u is the RoPE row pair (i, i + d/2), i = u % (d/2), of head
+ * slot u / (d/2); head slots are numbered KV group by KV group, each group g
+ * holding its `group` query heads g*group .. g*group+group-1, then K head g,
+ * then V head g.  A QKV task's units lie in one KV group, `aux`. */
 enum {
-  AMK_OP_QKV = 1,      /* RMSNorm + q/k/v GEMV of RoPE row-pair units [begin, end) + RoPE + KV append */
-  AMK_OP_ATTN = 2,     /* partial attention of KV head `aux`, position split `begin` of `end` */
+  AMK_OP_QKV = 1,      /* RMSNorm + q/k/v GEMV of units [begin, end) of KV group `aux` + RoPE + KV append */
+  AMK_OP_ATTN = 2,     /* attention of KV group `aux` over position split `begin` of `end` splits; queued
+                          splits leave partial results, the inline task (begin 0, end 1) the output */
   AMK_OP_COMBINE = 3,  /* merge the position splits of query heads [begin, end) (inline, see below) */
   AMK_OP_O = 4,        /* rows [begin, end) of x1 = x + Wo o */
   AMK_OP_GATEUP = 5,   /* rows [begin, end) of a = silu(Wg h2) * (Wu h2), h2 = RMSNorm(x1) */
@@ -209,7 +228,8 @@ enum {
 /* Queue value of an inline task: it runs on no queue of its own but at the
  * end of whichever producer of its single wait counter increments that
  * counter last (that producer's chain_counter names the inline task's
- * signal counter).  Used for the COMBINE of a KV group's attention splits. */
+ * signal counter).  Used for the ATTN of a KV group after its QKV tasks
+ * (short schedule) and for the COMBINE of its attention splits (long). */
 #define AMK_CU_INLINE (-1)
 
 /* Fixed-size task descriptor (64 bytes), the unit the device walks.  A task
@@ -255,24 +275,27 @@ enum {
   AMK_CHECK_INLINE = 10        /* an inline task or a chain counter that does not pair up */
 };
 
-/* Number of tasks / counters the schedule of cfg has on n_cu queues (after
- * validating cfg; tuning may be NULL).  Returns a status. */
-int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu,
+/* Number of tasks / counters schedule `variant` (AMK_SCHEDULE_*) of cfg has
+ * on n_cu queues (after validating cfg; tuning may be NULL).  Returns a
+ * status. */
+int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
                       int32_t* n_tasks, int32_t* n_counters);
 
 /* Lower cfg onto n_cu queues into tasks[cap] (cap >= n_tasks). */
-int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu,
+int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
                         amk_task_t* tasks, int32_t cap, int32_t* n_tasks, int32_t* n_counters);
 
 /* Check an arbitrary task array for cfg on n_cu queues with n_counters
  * counters.  Never fails for a bad schedule: the verdict is in *report
  * (report->ok); the return value is AMK_OK unless the arguments themselves
- * are unusable.  Accepted iff amk_create would launch it. */
+ * are unusable.  Accepted iff amk_create would launch it.  The rules do not
+ * depend on the variant. */
 int amk_schedule_check(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu,
                        const amk_task_t* tasks, int32_t n_tasks, int32_t n_counters,
                        amk_check_report_t* report);
 
-/* Validate cfg and build + check its schedule for n_cu queues (no device). */
+/* Validate cfg and build + check both schedule variants for n_cu queues (no
+ * device). */
 int amk_check_config(const amk_config_t* cfg, int32_t n_cu);
 
 #ifdef __cplusplus

@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libamk.so")
 
 # ---- constants (mirror include/amk.h) ---------------------------------------
-AMK_ABI_VERSION = 1
+AMK_ABI_VERSION = 2
 AMK_OK = 0
 AMK_ERR_INVALID_ARGUMENT = -1
 AMK_ERR_UNSUPPORTED = -2
@@ -29,12 +29,13 @@ AMK_ERR_ABORTED = -9
 AMK_WEIGHTS_BF16 = 0
 AMK_WEIGHTS_W8A16 = 1
 
+AMK_SCHEDULE_SHORT, AMK_SCHEDULE_LONG = 0, 1
 AMK_OP_QKV, AMK_OP_ATTN, AMK_OP_COMBINE, AMK_OP_O, AMK_OP_GATEUP, AMK_OP_DOWN, AMK_OP_LMHEAD, AMK_OP_ARGMAX = range(1, 9)
 AMK_MAX_WAITS = 4
 AMK_CU_INLINE = -1
 AMK_TRACE_FIELDS = 8
 (AMK_TRACE_WAIT_BEGIN, AMK_TRACE_WAIT_END, AMK_TRACE_INPUT_READY, AMK_TRACE_COMPUTE_END,
- AMK_TRACE_SIGNALLED, AMK_TRACE_PUBLISHED, AMK_TRACE_RELEASED, AMK_TRACE_SATISFIED) = range(8)
+ AMK_TRACE_SIGNALLED, AMK_TRACE_PUBLISHED, AMK_TRACE_CHAINED, AMK_TRACE_SATISFIED) = range(8)
 
 (AMK_CHECK_OK, AMK_CHECK_WELL_FORMED, AMK_CHECK_CAPACITY, AMK_CHECK_WAIT_SATISFIABLE, AMK_CHECK_ALL_JOIN,
  AMK_CHECK_ACYCLIC, AMK_CHECK_QUEUE_ORDER, AMK_CHECK_RACE, AMK_CHECK_KV_ORDER, AMK_CHECK_OUTPUT,
@@ -66,7 +67,7 @@ class amk_weights_t(ctypes.Structure):
 
 class amk_tuning_t(ctypes.Structure):
     _fields_ = [("attn_splits", ctypes.c_int32), ("timeout_us", ctypes.c_int32),
-                ("max_rows_per_task", ctypes.c_int32), ("trace", ctypes.c_int32)]
+                ("max_rows_per_task", ctypes.c_int32), ("trace", ctypes.c_int32), ("short_context", ctypes.c_int32)]
 
 
 class amk_task_t(ctypes.Structure):
@@ -114,14 +115,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "amk_reset": (ctypes.c_int, [ctypes.c_void_p]),
         "amk_set_abort": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
         "amk_status_string": (ctypes.c_char_p, [ctypes.c_int]),
-        "amk_schedule_size": (ctypes.c_int, [P(amk_config_t), P(amk_tuning_t), ctypes.c_int32, P(ctypes.c_int32),
-                                             P(ctypes.c_int32)]),
-        "amk_schedule_export": (ctypes.c_int, [P(amk_config_t), P(amk_tuning_t), ctypes.c_int32, P(amk_task_t),
-                                               ctypes.c_int32, P(ctypes.c_int32), P(ctypes.c_int32)]),
+        "amk_schedule_size": (ctypes.c_int, [P(amk_config_t), P(amk_tuning_t), ctypes.c_int32, ctypes.c_int32,
+                                             P(ctypes.c_int32), P(ctypes.c_int32)]),
+        "amk_schedule_export": (ctypes.c_int, [P(amk_config_t), P(amk_tuning_t), ctypes.c_int32, ctypes.c_int32,
+                                               P(amk_task_t), ctypes.c_int32, P(ctypes.c_int32), P(ctypes.c_int32)]),
         "amk_schedule_check": (ctypes.c_int, [P(amk_config_t), P(amk_tuning_t), ctypes.c_int32, P(amk_task_t),
                                               ctypes.c_int32, ctypes.c_int32, P(amk_check_report_t)]),
         "amk_check_config": (ctypes.c_int, [P(amk_config_t), ctypes.c_int32]),
-        "amk_trace_copy": (ctypes.c_int, [ctypes.c_void_p, P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_int32)]),
+        "amk_trace_copy": (ctypes.c_int, [ctypes.c_void_p, P(ctypes.c_uint64), ctypes.c_int64, P(ctypes.c_int32),
+                                          P(ctypes.c_int32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -183,26 +185,29 @@ def amk_set_abort(h, value: int) -> None:
 
 
 def amk_trace_copy(h, n_tasks: int):
-    """Per-task timestamps of the last step as a list of AMK_TRACE_FIELDS-tuples."""
+    """(variant, per-task timestamps) of the last step: a list of
+    AMK_TRACE_FIELDS-tuples in the order of that variant's export."""
     buf = (ctypes.c_uint64 * (n_tasks * AMK_TRACE_FIELDS))()
-    n = ctypes.c_int32()
-    _check(load().amk_trace_copy(h, buf, len(buf), ctypes.byref(n)), "amk_trace_copy")
-    return [tuple(buf[i * AMK_TRACE_FIELDS:(i + 1) * AMK_TRACE_FIELDS]) for i in range(n.value)]
+    n, v = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().amk_trace_copy(h, buf, len(buf), ctypes.byref(n), ctypes.byref(v)), "amk_trace_copy")
+    return v.value, [tuple(buf[i * AMK_TRACE_FIELDS:(i + 1) * AMK_TRACE_FIELDS]) for i in range(n.value)]
 
 
 def amk_check_config(cfg: amk_config_t, n_cu: int) -> int:
     return int(load().amk_check_config(ctypes.byref(cfg), n_cu))
 
 
-def amk_schedule_export(cfg: amk_config_t, n_cu: int, tuning: Optional[amk_tuning_t] = None):
+def amk_schedule_export(cfg: amk_config_t, n_cu: int, tuning: Optional[amk_tuning_t] = None,
+                        variant: int = AMK_SCHEDULE_LONG):
     """Returns (tasks array, n_counters) of the lowering of cfg onto n_cu queues."""
     lib = load()
     nt, nc = ctypes.c_int32(), ctypes.c_int32()
     tp = ctypes.byref(tuning) if tuning else None
-    _check(lib.amk_schedule_size(ctypes.byref(cfg), tp, n_cu, ctypes.byref(nt), ctypes.byref(nc)), "amk_schedule_size")
+    _check(lib.amk_schedule_size(ctypes.byref(cfg), tp, n_cu, variant, ctypes.byref(nt), ctypes.byref(nc)),
+           "amk_schedule_size")
     arr = (amk_task_t * nt.value)()
-    _check(lib.amk_schedule_export(ctypes.byref(cfg), tp, n_cu, arr, nt.value, ctypes.byref(nt), ctypes.byref(nc)),
-           "amk_schedule_export")
+    _check(lib.amk_schedule_export(ctypes.byref(cfg), tp, n_cu, variant, arr, nt.value, ctypes.byref(nt),
+                                   ctypes.byref(nc)), "amk_schedule_export")
     return arr, nc.value
 
 

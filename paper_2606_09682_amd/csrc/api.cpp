@@ -24,15 +24,29 @@ using amk::amk_internal_occupancy;
 using amk::amk_internal_prepare;
 using amk::amk_internal_threads;
 
+// One schedule variant as uploaded: device task table, queue offsets, trace.
+// Each variant owns its counters and epoch: a counter's target is
+// epoch * (its producers per launch), which holds only while every launch
+// that touched the counter ran the same schedule.
+struct DevSchedule {
+  const amk_task_t* tasks = nullptr;
+  const int32_t* queue_start = nullptr;
+  uint64_t* trace = nullptr;
+  uint32_t* counters = nullptr;
+  size_t counter_bytes = 0;
+  uint32_t epoch = 0;
+};
+
 struct amk_handle_s {
   Shape s;
   int device = 0;
-  Schedule sch;
+  Schedule sch[2];              // AMK_SCHEDULE_SHORT, AMK_SCHEDULE_LONG
+  DevSchedule dsch[2];
+  int last_variant = -1;
   DevModel dm;
   void* d_block = nullptr;      // one device allocation for tables and scratch
   int32_t* h_status = nullptr;  // host-mapped
   int32_t* h_abort = nullptr;   // host-mapped
-  uint32_t epoch = 0;
   void* last_stream = nullptr;
   bool launched = false;
   uint64_t timeout_ticks = 0;
@@ -99,13 +113,14 @@ size_t amk_kv_cache_bytes(const amk_config_t* cfg) {
   return (size_t)s.L * 2 * s.nkv * (size_t)s.max_seq * s.hd * 2;
 }
 
-int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t* n_tasks,
-                      int32_t* n_counters) {
+int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
+                      int32_t* n_tasks, int32_t* n_counters) {
+  if (variant != AMK_SCHEDULE_SHORT && variant != AMK_SCHEDULE_LONG) return AMK_ERR_INVALID_ARGUMENT;
   try {
     Shape s;
     int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
     if (st != AMK_OK) return st;
-    Schedule sch = amk::build_schedule(s, n_cu);
+    Schedule sch = amk::build_schedule(s, n_cu, variant);
     if (n_tasks) *n_tasks = (int32_t)sch.tasks.size();
     if (n_counters) *n_counters = sch.n_counters;
     return AMK_OK;
@@ -116,13 +131,14 @@ int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32
   }
 }
 
-int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, amk_task_t* tasks,
-                        int32_t cap, int32_t* n_tasks, int32_t* n_counters) {
+int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
+                        amk_task_t* tasks, int32_t cap, int32_t* n_tasks, int32_t* n_counters) {
+  if (variant != AMK_SCHEDULE_SHORT && variant != AMK_SCHEDULE_LONG) return AMK_ERR_INVALID_ARGUMENT;
   try {
     Shape s;
     int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
     if (st != AMK_OK) return st;
-    Schedule sch = amk::build_schedule(s, n_cu);
+    Schedule sch = amk::build_schedule(s, n_cu, variant);
     if (n_tasks) *n_tasks = (int32_t)sch.tasks.size();
     if (n_counters) *n_counters = sch.n_counters;
     if (!tasks || cap < (int32_t)sch.tasks.size()) return AMK_ERR_INVALID_ARGUMENT;
@@ -156,10 +172,12 @@ int amk_check_config(const amk_config_t* cfg, int32_t n_cu) {
     Shape s;
     int st = amk::derive_shape(cfg, nullptr, n_cu, &s, nullptr);
     if (st != AMK_OK) return st;
-    Schedule sch = amk::build_schedule(s, n_cu);
-    amk_check_report_t rep;
-    if (!amk::check_schedule(s, n_cu, sch.tasks.data(), (int)sch.tasks.size(), sch.n_counters, &rep))
-      return AMK_ERR_SCHEDULE_REJECTED;
+    for (int v = AMK_SCHEDULE_SHORT; v <= AMK_SCHEDULE_LONG; ++v) {
+      Schedule sch = amk::build_schedule(s, n_cu, v);
+      amk_check_report_t rep;
+      if (!amk::check_schedule(s, n_cu, sch.tasks.data(), (int)sch.tasks.size(), sch.n_counters, &rep))
+        return AMK_ERR_SCHEDULE_REJECTED;
+    }
     return AMK_OK;
   } catch (const std::bad_alloc&) {
     return AMK_ERR_OUT_OF_MEMORY;
@@ -212,10 +230,18 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     h = new amk_handle_s();
     h->s = s;
     h->device = dev;
-    h->sch = amk::build_schedule(s, n_cu);
-    amk_check_report_t rep;
-    if (!amk::check_schedule(s, n_cu, h->sch.tasks.data(), (int)h->sch.tasks.size(), h->sch.n_counters, &rep)) {
-      std::fprintf(stderr, "amk: schedule rejected (rule %d): %s\n", rep.rule, rep.message);
+    for (int v = AMK_SCHEDULE_SHORT; v <= AMK_SCHEDULE_LONG; ++v) {
+      h->sch[v] = amk::build_schedule(s, n_cu, v);
+      amk_check_report_t rep;
+      if (!amk::check_schedule(s, n_cu, h->sch[v].tasks.data(), (int)h->sch[v].tasks.size(), h->sch[v].n_counters,
+                               &rep)) {
+        std::fprintf(stderr, "amk: schedule variant %d rejected (rule %d): %s\n", v, rep.rule, rep.message);
+        free_handle(h);
+        return AMK_ERR_SCHEDULE_REJECTED;
+      }
+    }
+    const Schedule& sl = h->sch[AMK_SCHEDULE_LONG];
+    if (sl.n_lm_slots != h->sch[AMK_SCHEDULE_SHORT].n_lm_slots) {  // the argmax slots are shared
       free_handle(h);
       return AMK_ERR_SCHEDULE_REJECTED;
     }
@@ -224,8 +250,10 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     // static per-row data, residual rows, partials / attention scratch
     const int nsw = amk_internal_threads() / 64 - 1;
     const size_t act = round_up((size_t)std::max({s.H, s.nq * s.hd, s.I}), 1024);
-    const size_t scr = std::max<size_t>((size_t)nsw * s.max_jobs, (size_t)amk_internal_attn_scratch(s.group, s.hd));
-    const size_t lds_bytes = (act + s.H + 3 * (size_t)s.max_jobs + scr) * 4;
+    // per-wave partial stride in whole float4s keeps every region 16-byte aligned
+    const size_t pstride = round_up((size_t)s.max_jobs, 4);
+    const size_t scr = std::max<size_t>((size_t)nsw * pstride, (size_t)amk_internal_attn_scratch(s.group, s.hd));
+    const size_t lds_bytes = (act + s.H + 3 * pstride + scr) * 4;
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
       free_handle(h);
@@ -248,7 +276,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
 
     // device block layout
     const int L = s.L;
-    const int n_lm = h->sch.n_lm_slots;
+    const int n_lm = sl.n_lm_slots;
     const int rec = s.group * (amk::kPartHead + s.hd);
     struct Region { size_t off, bytes; };
     size_t top = 0;
@@ -262,12 +290,15 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     const Region r_a = take(sizeof(float) * (size_t)L * s.I);
     const Region r_argp = take(sizeof(float) * 2 * n_lm);
     const Region r_next = take(sizeof(int32_t));
-    const Region r_ctr = take(sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch.n_counters);
     const Region r_abort = take(sizeof(int32_t));
-    const Region r_tasks = take(sizeof(amk_task_t) * h->sch.tasks.size());
-    const Region r_queue = take(sizeof(int32_t) * h->sch.queue_start.size());
     const bool tracing = tuning && tuning->trace;
-    const Region r_trace = take(tracing ? sizeof(uint64_t) * AMK_TRACE_FIELDS * h->sch.tasks.size() : 0);
+    Region r_tasks[2], r_queue[2], r_trace[2], r_ctr[2];
+    for (int v = 0; v < 2; ++v) {
+      r_ctr[v] = take(sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch[v].n_counters);
+      r_tasks[v] = take(sizeof(amk_task_t) * h->sch[v].tasks.size());
+      r_queue[v] = take(sizeof(int32_t) * h->sch[v].queue_start.size());
+      r_trace[v] = take(tracing ? sizeof(uint64_t) * AMK_TRACE_FIELDS * h->sch[v].tasks.size() : 0);
+    }
     if (hipMalloc(&h->d_block, top) != hipSuccess) {
       h->d_block = nullptr;
       free_handle(h);
@@ -318,11 +349,12 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       }
     }
     bool ok = hipMemcpy(base + r_layers.off, layers.data(), r_layers.bytes, hipMemcpyHostToDevice) == hipSuccess &&
-              hipMemcpy(base + r_rope.off, rope.data(), r_rope.bytes, hipMemcpyHostToDevice) == hipSuccess &&
-              hipMemcpy(base + r_tasks.off, h->sch.tasks.data(), r_tasks.bytes, hipMemcpyHostToDevice) ==
-                  hipSuccess &&
-              hipMemcpy(base + r_queue.off, h->sch.queue_start.data(), r_queue.bytes, hipMemcpyHostToDevice) ==
-                  hipSuccess;
+              hipMemcpy(base + r_rope.off, rope.data(), r_rope.bytes, hipMemcpyHostToDevice) == hipSuccess;
+    for (int v = 0; v < 2 && ok; ++v)
+      ok = hipMemcpy(base + r_tasks[v].off, h->sch[v].tasks.data(), r_tasks[v].bytes, hipMemcpyHostToDevice) ==
+               hipSuccess &&
+           hipMemcpy(base + r_queue[v].off, h->sch[v].queue_start.data(), r_queue[v].bytes, hipMemcpyHostToDevice) ==
+               hipSuccess;
     if (!ok) {
       free_handle(h);
       return AMK_ERR_DEVICE;
@@ -337,6 +369,8 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.half_log2 = 0;
     while ((1 << m.half_log2) < s.half) ++m.half_log2;
     m.units = s.units; m.q_units = s.q_units; m.nsplit = s.nsplit; m.n_lm = n_lm;
+    m.gq2 = s.group + 2;
+    m.npg = s.npg;
     m.n_cu = n_cu;
     m.eps = s.eps;
     m.attn_scale = (float)(1.0 / std::sqrt((double)s.hd));
@@ -353,15 +387,19 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.a = (float*)(base + r_a.off);
     m.argp = (float*)(base + r_argp.off);
     m.next_token = (int32_t*)(base + r_next.off);
-    m.counters = (uint32_t*)(base + r_ctr.off);
+    m.counters = nullptr;  // per launch: the variant's counters
     m.dev_abort = (int32_t*)(base + r_abort.off);
     m.host_status = d_status;
     m.host_abort = d_hab;
-    m.trace = tracing ? (uint64_t*)(base + r_trace.off) : nullptr;
-    m.tasks = (const amk_task_t*)(base + r_tasks.off);
-    m.queue_start = (const int32_t*)(base + r_queue.off);
+    for (int v = 0; v < 2; ++v) {
+      h->dsch[v].tasks = (const amk_task_t*)(base + r_tasks[v].off);
+      h->dsch[v].queue_start = (const int32_t*)(base + r_queue[v].off);
+      h->dsch[v].trace = tracing ? (uint64_t*)(base + r_trace[v].off) : nullptr;
+      h->dsch[v].counters = (uint32_t*)(base + r_ctr[v].off);
+      h->dsch[v].counter_bytes = r_ctr[v].bytes;
+    }
     m.lds_act = (int32_t)act;
-    m.part_stride = s.max_jobs;
+    m.part_stride = (int32_t)pstride;
     m.lds_scr = (int32_t)scr;
     m.lds_bytes = (int32_t)lds_bytes;
 
@@ -386,11 +424,18 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   if (sticky != 0) return sticky;
   DeviceGuard guard(h->device);
   if (!guard.ok) return AMK_ERR_DEVICE;
-  const uint32_t epoch = h->epoch + 1;  // counter targets are epoch * producers, mod 2^32
-  const int st = amk_internal_launch(&h->dm, token, pos, epoch, (uint16_t*)kv_cache, logits, h->timeout_ticks,
-                                     stream);
+  const int variant = pos + 1 <= h->s.short_context ? AMK_SCHEDULE_SHORT : AMK_SCHEDULE_LONG;
+  DevSchedule& ds = h->dsch[variant];
+  DevModel m = h->dm;
+  m.tasks = ds.tasks;
+  m.queue_start = ds.queue_start;
+  m.trace = ds.trace;
+  m.counters = ds.counters;
+  const uint32_t epoch = ds.epoch + 1;  // counter targets are epoch * producers, mod 2^32
+  const int st = amk_internal_launch(&m, token, pos, epoch, (uint16_t*)kv_cache, logits, h->timeout_ticks, stream);
   if (st != AMK_OK) return st;
-  h->epoch = epoch;
+  h->last_variant = variant;
+  ds.epoch = epoch;
   h->last_stream = stream;
   h->launched = true;
   return AMK_OK;
@@ -419,24 +464,27 @@ int amk_reset(amk_handle_t h) {
   if (!h) return AMK_ERR_INVALID_ARGUMENT;
   DeviceGuard guard(h->device);
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
-  const size_t ctr_bytes = sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch.n_counters;
-  if (hipMemset(h->dm.counters, 0, ctr_bytes) != hipSuccess) return AMK_ERR_DEVICE;
+  for (auto& ds : h->dsch) {
+    if (hipMemset(ds.counters, 0, ds.counter_bytes) != hipSuccess) return AMK_ERR_DEVICE;
+    ds.epoch = 0;
+  }
   if (hipMemset(h->dm.dev_abort, 0, sizeof(int32_t)) != hipSuccess) return AMK_ERR_DEVICE;
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
   *(volatile int32_t*)h->h_status = 0;
-  h->epoch = 0;
   return AMK_OK;
 }
 
-int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks) {
+int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks, int32_t* variant) {
   if (!h || !dst) return AMK_ERR_INVALID_ARGUMENT;
-  if (!h->dm.trace) return AMK_ERR_BAD_STATE;
-  const size_t n = h->sch.tasks.size();
+  if (h->last_variant < 0 || !h->dsch[h->last_variant].trace) return AMK_ERR_BAD_STATE;
+  const int v = h->last_variant;
+  const size_t n = h->sch[v].tasks.size();
   if (n_tasks) *n_tasks = (int32_t)n;
+  if (variant) *variant = v;
   if (capacity < (int64_t)(n * AMK_TRACE_FIELDS)) return AMK_ERR_INVALID_ARGUMENT;
   DeviceGuard guard(h->device);
   if (h->launched && hipStreamSynchronize((hipStream_t)h->last_stream) != hipSuccess) return AMK_ERR_DEVICE;
-  if (hipMemcpy(dst, h->dm.trace, n * AMK_TRACE_FIELDS * sizeof(uint64_t), hipMemcpyDeviceToHost) != hipSuccess)
+  if (hipMemcpy(dst, h->dsch[v].trace, n * AMK_TRACE_FIELDS * sizeof(uint64_t), hipMemcpyDeviceToHost) != hipSuccess)
     return AMK_ERR_DEVICE;
   return AMK_OK;
 }

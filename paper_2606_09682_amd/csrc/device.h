@@ -31,6 +31,8 @@ struct DevModel {
   int32_t fmt;        // AMK_WEIGHTS_*
   int32_t lm_int8;    // LM head stored as int8 + scales (untied W8A16)
   int32_t group, half, half_log2, units, q_units, nsplit, n_lm;
+  int32_t gq2;        // group + 2: head slots of one KV group in QKV unit order
+  int32_t npg;        // QKV tasks per KV group (producers of a group's QKV counter)
   int32_t n_cu;
   float eps;
   float attn_scale;   // 1 / sqrt(head_dim)
@@ -53,6 +55,7 @@ struct DevModel {
   int32_t* dev_abort;        // device word: nonzero stops every workgroup at its next wait
   int32_t* host_status;      // host-mapped: first device error code
   const int32_t* host_abort; // host-mapped: raised by amk_set_abort
+  // schedule of this launch (one of the handle's variants)
   uint64_t* trace;           // [n_tasks][AMK_TRACE_FIELDS] timestamps, or null
   const amk_task_t* tasks;   // sorted by (cu, seq)
   const int32_t* queue_start;// [n_cu + 1]

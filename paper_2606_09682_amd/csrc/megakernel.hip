@@ -13,13 +13,19 @@
 //               16-byte-per-lane vectors through a double-buffered register
 //               pipeline and reduce them against the LDS activation.
 //   all waves   load the task's input activation into LDS after the wait (one
-//               round trip) and run the attention tasks.
+//               round trip), run attention, and run inline continuations.
 //
 // Per task the workgroup passes four barriers:
 //   B1a  the sync wave's counter wait is satisfied (or the launch aborts)
-//   B1b  the input activation is in LDS
-//   B2   the task's compute is done (partials / attention output in LDS)
+//   B1b  the input activation is in LDS (GEMV tasks)
+//   B2   the task's compute is done (partials in LDS / attention stored)
 //   B3   the sync wave has stored, released and signalled the task's results
+// A task with a chain counter whose signal completed its counter (it is the
+// last producer of this launch) then runs that counter's inline task with
+// every wave: a KV group's whole attention after its QKV tasks, or the merge
+// of a KV group's attention splits.  Each wave drains its own stores, the
+// workgroup meets at B4, the sync wave releases and signals the chain
+// counter, and B5 keeps the next task's weight loads behind that signal.
 // The streaming waves issue the weight loads of their NEXT task right after
 // B3.  Memory requests of one CU are served roughly in order, so loads issued
 // before the result stores, the release or the counter increment would delay
@@ -51,8 +57,8 @@ constexpr int GRAN = 1024;    // bytes per wave-wide 16-B-per-lane load
 
 struct Ctl {
   int abort;
+  int cont;                     // this task runs its chain counter's inline task
   int res_buf, res_lo, res_hi;  // residual rows cached in LDS: x buffer index and row range
-  float m_run[8], l_run[8], alpha[8];
   float ssq[NW];                // per-wave sum of squares of the task input
 };
 
@@ -99,6 +105,11 @@ __device__ __forceinline__ uint16_t f2bf(float f) {  // round to nearest even
 }
 __device__ __forceinline__ float i8f(uint32_t w, int k) { return (float)(int8_t)(w >> (8 * k)); }
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+// Wait until every global load and store this wave issued has completed
+// (s_waitcnt vmcnt(0)).  A barrier does not wait for them, so waves that
+// store results another CU reads drain before the barrier that precedes the
+// sync wave's agent-scope release.
+__device__ __forceinline__ void drain_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // DPP lane moves.  Control codes: quad_perm [1,0,3,2] = 0xb1, [2,3,0,1] = 0x4e,
 // row_mirror = 0x140, row_half_mirror = 0x141, row_bcast15 = 0x142,
@@ -162,16 +173,24 @@ struct Gemv {
   int G;           // total granules = nj * gpr
 };
 
+// QKV unit u: head slot u / (d/2) counts KV group by KV group, each group
+// holding its query heads, then its K head, then its V head.
+__device__ __forceinline__ void unit_head(const DevModel& m, int u, int* mat, int* head) {
+  const int slot = u >> m.half_log2;
+  const int g = slot / m.gq2;
+  const int r = slot - g * m.gq2;
+  if (r < m.group) { *mat = W_Q; *head = g * m.group + r; }
+  else { *mat = r == m.group ? W_K : W_V; *head = g; }
+}
+
 // Which matrix and row job j of task t reads.  mat < 0 means the LM head.
 __device__ __forceinline__ void job_row(const DevModel& m, const amk_task_t& t, int j, int* mat, int* row) {
   switch (t.op) {
     case AMK_OP_QKV: {
       const int u = t.begin + (j >> 1);
-      const int hh = u >> m.half_log2;
-      const int r = (u & (m.half - 1)) + (j & 1) * m.half;
-      if (hh < m.nq) { *mat = W_Q; *row = hh * m.hd + r; }
-      else if (hh < m.nq + m.nkv) { *mat = W_K; *row = (hh - m.nq) * m.hd + r; }
-      else { *mat = W_V; *row = (hh - m.nq - m.nkv) * m.hd + r; }
+      int head;
+      unit_head(m, u, mat, &head);
+      *row = head * m.hd + (u & (m.half - 1)) + (j & 1) * m.half;
       break;
     }
     case AMK_OP_GATEUP: *mat = (j & 1) ? W_U : W_G; *row = t.begin + (j >> 1); break;
@@ -199,7 +218,6 @@ __device__ __forceinline__ int task_k(const DevModel& m, const amk_task_t& t) {
   switch (t.op) {
     case AMK_OP_O: return m.nq * m.hd;
     case AMK_OP_DOWN: return m.I;
-    case AMK_OP_ATTN: return m.group * m.hd;
     default: return m.H;
   }
 }
@@ -216,8 +234,9 @@ __device__ __forceinline__ Gemv gemv_geom(const DevModel& m, const amk_task_t& t
   return g;
 }
 
-// Granule range of streaming wave sw: [sw*G/NSW, (sw+1)*G/NSW).
-__device__ __forceinline__ int wave_gbegin(int G, int sw) { return (int)(((long)G * sw) / NSW); }
+// Granule range of streaming wave sw: [sw*G/NSW, (sw+1)*G/NSW).  G * NSW
+// stays far below 2^31 (rows per task <= 1024, granules per row <= 64).
+__device__ __forceinline__ int wave_gbegin(int G, int sw) { return (G * sw) / NSW; }
 
 struct Cursor {
   int j, c;
@@ -461,7 +480,6 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
     case AMK_OP_LMHEAD: src = m.x + (size_t)(2 * m.L) * m.H; break;
     case AMK_OP_O: src = m.o + (size_t)t.layer * m.nq * m.hd; break;
     case AMK_OP_DOWN: src = m.a + (size_t)t.layer * m.I; break;
-    case AMK_OP_ATTN: src = m.q + (size_t)t.layer * m.nq * m.hd + (size_t)t.aux * m.group * m.hd; break;
     default: return;
   }
   const int K = task_k(m, t);
@@ -512,12 +530,23 @@ __device__ __forceinline__ float input_rs(const DevModel& m, const Ctl& ctl) {
 }
 
 // ---------------------------------------------------------------- row sums of a GEMV task
-__device__ __forceinline__ float row_sum(const float* part, int stride, const Gemv& g, int j) {
+// Granule boundaries of the streaming waves, computed once per epilogue.
+struct Ranges {
+  int b[NSW + 1];
+};
+__device__ __forceinline__ Ranges wave_ranges(const Gemv& g) {
+  Ranges r;
+#pragma unroll
+  for (int sw = 0; sw <= NSW; ++sw) r.b[sw] = wave_gbegin(g.G, sw);
+  return r;
+}
+
+__device__ __forceinline__ float row_sum(const float* part, int stride, const Gemv& g, const Ranges& wr, int j) {
   float s = 0.f;
   const int lo = j * g.gpr, hi = lo + g.gpr;
 #pragma unroll
   for (int sw = 0; sw < NSW; ++sw) {
-    const int gb = wave_gbegin(g.G, sw), ge = wave_gbegin(g.G, sw + 1);
+    const int gb = wr.b[sw], ge = wr.b[sw + 1];
     // a wave with an empty range wrote nothing, even if gb lies inside the row
     if (gb < ge && gb < hi && ge > lo) s += part[sw * stride + j];
   }
@@ -528,17 +557,18 @@ __device__ __forceinline__ float row_sum(const float* part, int stride, const Ge
 __device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L, int pos,
                                         uint16_t* kv, float rs, int lane) {
   const int l = t.layer;
+  const Ranges wr = wave_ranges(g);
   for (int u = t.begin + lane; u < t.end; u += 64) {
     const int j0 = 2 * (u - t.begin);
-    float y0 = row_sum(L.part, m.part_stride, g, j0) * rs;
-    float y1 = row_sum(L.part, m.part_stride, g, j0 + 1) * rs;
+    float y0 = row_sum(L.part, m.part_stride, g, wr, j0) * rs;
+    float y1 = row_sum(L.part, m.part_stride, g, wr, j0 + 1) * rs;
     if (g.int8) {
       y0 *= L.stat[j0];
       y1 *= L.stat[j0 + 1];
     }
-    const int hh = u >> m.half_log2;
+    int mat, head;
+    unit_head(m, u, &mat, &head);
     const int i = u & (m.half - 1);
-    const int mat = hh < m.nq ? W_Q : hh < m.nq + m.nkv ? W_K : W_V;
     if (mat != W_V) {
       const float c = L.stat[g.nj + 2 * (u - t.begin)], s = L.stat[g.nj + 2 * (u - t.begin) + 1];
       const float a = y0 * c - y1 * s;
@@ -547,13 +577,12 @@ __device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, 
       y1 = b;
     }
     if (mat == W_Q) {
-      float* qd = m.q + (size_t)l * m.nq * m.hd + (size_t)hh * m.hd;
+      float* qd = m.q + (size_t)l * m.nq * m.hd + (size_t)head * m.hd;
       stg<float>(qd + i, y0);
       stg<float>(qd + i + m.half, y1);
     } else {
-      const int kvh = (mat == W_K) ? hh - m.nq : hh - m.nq - m.nkv;
       const int which = (mat == W_K) ? 0 : 1;
-      uint16_t* dst = kv + (((size_t)(l * 2 + which) * m.nkv + kvh) * m.max_seq + pos) * m.hd;
+      uint16_t* dst = kv + (((size_t)(l * 2 + which) * m.nkv + head) * m.max_seq + pos) * m.hd;
       stg<uint16_t>(dst + i, f2bf(y0));
       stg<uint16_t>(dst + i + m.half, f2bf(y1));
     }
@@ -566,8 +595,9 @@ __device__ __forceinline__ void epi_residual(const DevModel& m, const amk_task_t
                                              Ctl& ctl, int lane) {
   const int xin = t.op == AMK_OP_O ? 2 * t.layer : 2 * t.layer + 1;
   const bool cached = ctl.res_buf == xin && ctl.res_lo == t.begin && ctl.res_hi == t.end;
+  const Ranges wr = wave_ranges(g);
   for (int r = t.begin + lane; r < t.end; r += 64) {
-    float y = row_sum(L.part, m.part_stride, g, r - t.begin);
+    float y = row_sum(L.part, m.part_stride, g, wr, r - t.begin);
     if (g.int8) y *= L.stat[r - t.begin];
     const float x = cached ? L.res[r - t.begin] : ldg<float>(m.x + (size_t)xin * m.H + r);
     const float o = x + y;
@@ -583,10 +613,11 @@ __device__ __forceinline__ void epi_residual(const DevModel& m, const amk_task_t
 
 __device__ __forceinline__ void epi_gateup(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L,
                                            float rs, int lane) {
+  const Ranges wr = wave_ranges(g);
   for (int r = t.begin + lane; r < t.end; r += 64) {
     const int j = 2 * (r - t.begin);
-    float gv = row_sum(L.part, m.part_stride, g, j) * rs;
-    float uv = row_sum(L.part, m.part_stride, g, j + 1) * rs;
+    float gv = row_sum(L.part, m.part_stride, g, wr, j) * rs;
+    float uv = row_sum(L.part, m.part_stride, g, wr, j + 1) * rs;
     if (g.int8) {
       gv *= L.stat[j];
       uv *= L.stat[j + 1];
@@ -601,8 +632,9 @@ __device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& 
                                            float rs, float* logits, int lane) {
   float best = -INFINITY;
   int besti = 0x7fffffff;
+  const Ranges wr = wave_ranges(g);
   for (int r = t.begin + lane; r < t.end; r += 64) {
-    float y = row_sum(L.part, m.part_stride, g, r - t.begin) * rs;
+    float y = row_sum(L.part, m.part_stride, g, wr, r - t.begin) * rs;
     if (g.int8) y *= L.stat[r - t.begin];
     stg<float>(logits + r, y);
     if (y > best || (y == best && r < besti)) { best = y; besti = r; }
@@ -614,34 +646,6 @@ __device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& 
     if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
   }
   if (lane == 0) stg<float2>(m.argp + 2 * t.aux, make_float2(best, __int_as_float(besti)));
-}
-
-// Merge the position splits of query heads [h0, h1) (flash-decoding style).
-__device__ __forceinline__ void combine_heads(const DevModel& m, int l, int h0, int h1, int pos, int lane) {
-  const int n_pos = pos + 1;
-  const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
-  const int active = (n_pos + chunk - 1) / chunk;
-  const int rec = m.group * (kPartHead + m.hd);
-  for (int h = h0; h < h1; ++h) {
-    const int g = h / m.group, hg = h - g * m.group;
-    const float* base = m.part + ((size_t)(l * m.nkv + g) * m.nsplit) * rec + hg * (kPartHead + m.hd);
-    float ms = -INFINITY, ls = 0.f;
-    if (lane < active) {
-      const float2 ml = ldg<float2>(base + (size_t)lane * rec);
-      ms = ml.x;
-      ls = ml.y;
-    }
-    const float M = wave_max(ms);
-    const float w = lane < active ? __expf(ms - M) : 0.f;
-    const float inv = 1.0f / wave_sum(w * ls);
-    float* dst = m.o + (size_t)l * m.nq * m.hd + (size_t)h * m.hd;
-    for (int d = lane; d < m.hd; d += 64) {
-      float acc = 0.f;
-      for (int s = 0; s < active; ++s)
-        acc = fmaf(__shfl(w, s), ldg<float>(base + (size_t)s * rec + kPartHead + d), acc);
-      stg<float>(dst + d, acc * inv);
-    }
-  }
 }
 
 __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t& t, int lane) {
@@ -662,21 +666,25 @@ __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t
 }
 
 // ---------------------------------------------------------------- attention (all 8 waves)
-// Geometry of the attention split of one task, shared with the host's LDS
-// sizing.  HD: head dim; GM: largest query group handled (accumulators per
-// lane = GM * EPL); EPL: head dims per lane (8 for groups <= 4, 4 for groups
-// <= 8 to halve the accumulators); LPR lanes cover one K/V row, RPW rows per
-// wave-wide load, RP rows per pass of the workgroup, KB rows per lane per
-// sub-chunk of SC rows.
+// Geometry of the attention of one KV group, shared with the host's LDS
+// sizing.  HD: head dim; GM: largest query group handled; EPL: head dims per
+// lane (8 for groups <= 4, 4 for groups <= 8 to halve the accumulators); LPR
+// lanes cover one K/V row, RPW rows per wave-wide load; each lane holds KB K
+// rows and KB V rows per pass, so a pass of the workgroup covers RP rows with
+// all its loads in flight at once.
 template <int HD, int GM>
 struct AttnGeom {
   static constexpr int EPL = GM <= 4 ? 8 : 4;
   static constexpr int LPR = HD / EPL;
   static constexpr int RPW = 64 / LPR;
-  static constexpr int RP = NW * RPW;
-  static constexpr int KB = GM <= 4 ? 8 : 4;
-  static constexpr int SC = RP * KB;
-  static constexpr int SCRATCH = GM * SC + NW * GM * HD + GM * HD;  // floats
+  static constexpr int KB = 9;
+  static constexpr int SB = 3;  // rows per lane per softmax update
+  static constexpr int RP = NW * RPW * KB;
+  // LDS scratch (floats): per-wave accumulators red[NW][GM][HD] and running
+  // (max, sum) stat[NW][GM][2]; the split merge reuses the region
+  static constexpr int SCRATCH = NW * GM * HD + 2 * NW * GM;
+  static constexpr int MERGE = GM * 64 + 4 * NT;
+  static constexpr int LDS = SCRATCH > MERGE ? SCRATCH : MERGE;
   static_assert(LPR >= 2 && LPR <= 32, "lanes per row");
 };
 
@@ -702,140 +710,177 @@ __device__ __forceinline__ float row_elem(const RowVec<EPL>& r, int e) {
   return (e & 1) ? bf_hi(w) : bf_lo(w);
 }
 
-// Partial attention of query group `t.aux` over position split t.begin of
-// t.end: scores, running max / sum (online softmax) and the V-weighted sum.
-// Leaves out[G][HD] (unnormalised) in scratch and (m, l) per head in ctl.
+// Attention of the query heads of KV group g over positions [j0, j1) of
+// layer `layer` (j1 > j0), scores q.k / sqrt(d), max-subtracted softmax,
+// V-weighted sum (paper §2 "Kernel authoring and attention" names the
+// flash-decoding family this follows).  Every wave keeps its own running
+// max / sum / accumulators over the rows it loads (online softmax, no
+// barrier inside the position loop); the waves merge through LDS at the end.
+// `record`: store per head (m, l, unnormalised acc) at dst[h * (kPartHead +
+// d)], else the normalised output at dst[h * d].  Stores are issued by every
+// wave; the caller drains them.
 template <int HD, int GM>
-__device__ __forceinline__ void attention(const DevModel& m, const amk_task_t& t, int pos,
-                                          const uint16_t* __restrict__ kv, const float* __restrict__ q,
-                                          float* __restrict__ scr, Ctl& ctl, int wave, int lane) {
+__device__ __forceinline__ void attention(const DevModel& m, int layer, int g, int j0, int j1,
+                                          const uint16_t* __restrict__ kv, float* __restrict__ qs,
+                                          float* __restrict__ scr, float* __restrict__ dst, bool record, int wave,
+                                          int lane) {
   using A = AttnGeom<HD, GM>;
-  constexpr int EPL = A::EPL, LPR = A::LPR, RPW = A::RPW, RP = A::RP, KB = A::KB, SC = A::SC;
+  constexpr int EPL = A::EPL, LPR = A::LPR, RPW = A::RPW, KB = A::KB, SB = A::SB, RP = A::RP;
+  static_assert(KB % SB == 0, "sub-batches");
   const int G = m.group;
-  const int n_pos = pos + 1;
-  const int chunk = (n_pos + m.nsplit - 1) / m.nsplit;
-  const int j0 = t.begin * chunk;
-  const int j1 = min(n_pos, j0 + chunk);
+  const int n = j1 - j0;
   const int sub = lane / LPR, c = lane % LPR;
   const size_t hs = (size_t)m.max_seq * HD;
-  const uint16_t* Kp = kv + ((size_t)(t.layer * 2 + 0) * m.nkv + t.aux) * hs + c * EPL;
-  const uint16_t* Vp = kv + ((size_t)(t.layer * 2 + 1) * m.nkv + t.aux) * hs + c * EPL;
-  float* sc = scr;                  // [GM][SC]
-  float* red = scr + GM * SC;       // [NW][GM][HD]
-  float* out = red + NW * GM * HD;  // [G][HD]
+  const uint16_t* Kp = kv + ((size_t)(layer * 2 + 0) * m.nkv + g) * hs + (size_t)j0 * HD + c * EPL;
+  const uint16_t* Vp = kv + ((size_t)(layer * 2 + 1) * m.nkv + g) * hs + (size_t)j0 * HD + c * EPL;
 
-  if (threadIdx.x < 8) {
-    ctl.m_run[threadIdx.x] = -INFINITY;
-    ctl.l_run[threadIdx.x] = 0.f;
-  }
-  float acc[GM][EPL];
+  float m_run[GM], l_run[GM], acc[GM][EPL];
 #pragma unroll
-  for (int h = 0; h < GM; ++h)
+  for (int h = 0; h < GM; ++h) {
+    m_run[h] = -INFINITY;
+    l_run[h] = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[h][e] = 0.f;
-  __syncthreads();
+  }
 
-  for (int t0 = j0; t0 < j1; t0 += SC) {
-    const int n = min(SC, j1 - t0);
+  for (int p0 = 0; p0 < n; p0 += RP) {
+    // rows of this lane: r_k = p0 + (k * NW + wave) * RPW + sub
     RowVec<EPL> kr[KB], vr[KB];
 #pragma unroll
     for (int k = 0; k < KB; ++k) {
-      const int r = wave * RPW + sub + k * RP;
+      const int r = p0 + (k * NW + wave) * RPW + sub;
       zero_row<EPL>(kr[k]);
-      if (r < n) kr[k] = load_row<EPL>(Kp + (size_t)(t0 + r) * HD);
-    }
-    // scores s_j = q_h . k_j / sqrt(d) for the group's query heads
-#pragma unroll
-    for (int k = 0; k < KB; ++k) {
-      const int r = wave * RPW + sub + k * RP;
-#pragma unroll
-      for (int h = 0; h < GM; ++h) {
-        if (h < G) {
-          const float* qh = q + h * HD + c * EPL;
-          float d = 0.f;
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) d = fmaf(row_elem<EPL>(kr[k], e), qh[e], d);
-          d = group_sum<LPR>(d);
-          if (c == 0 && r < n) sc[h * SC + r] = d * m.attn_scale;
-        }
-      }
-    }
-    // V rows do not depend on the scores: their loads overlap the softmax statistics below
-#pragma unroll
-    for (int k = 0; k < KB; ++k) {
-      const int r = wave * RPW + sub + k * RP;
       zero_row<EPL>(vr[k]);
-      if (r < n) vr[k] = load_row<EPL>(Vp + (size_t)(t0 + r) * HD);
-    }
-    __syncthreads();
-    // running max / sum per head (wave h handles head h)
-    if (wave < G) {
-      const int h = wave;
-      float mx = -INFINITY;
-      for (int r = lane; r < n; r += 64) mx = fmaxf(mx, sc[h * SC + r]);
-      mx = wave_max(mx);
-      const float m_old = ctl.m_run[h];
-      const float m_new = fmaxf(m_old, mx);
-      float sum = 0.f;
-      for (int r = lane; r < n; r += 64) {
-        const float p = __expf(sc[h * SC + r] - m_new);
-        sc[h * SC + r] = p;
-        sum += p;
-      }
-      sum = wave_sum(sum);
-      if (lane == 0) {
-        const float alpha = __expf(m_old - m_new);
-        ctl.alpha[h] = alpha;
-        ctl.l_run[h] = ctl.l_run[h] * alpha + sum;
-        ctl.m_run[h] = m_new;
-      }
-    }
-    __syncthreads();
-    // V accumulation with the rescaled running sums
-#pragma unroll
-    for (int h = 0; h < GM; ++h) {
-      if (h < G) {
-        const float al = ctl.alpha[h];
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[h][e] *= al;
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < KB; ++k) {
-      const int r = wave * RPW + sub + k * RP;
       if (r < n) {
+        kr[k] = load_row<EPL>(Kp + (size_t)r * HD);
+        vr[k] = load_row<EPL>(Vp + (size_t)r * HD);
+      }
+    }
+    if (p0 == 0) {
+      // the group's roped queries into LDS while the first rows are in flight
+      const float* qsrc = m.q + ((size_t)layer * m.nq + (size_t)g * G) * HD;
+      for (int i = threadIdx.x; i < G * HD / 4; i += NT)
+        *reinterpret_cast<float4*>(qs + 4 * i) = ldg<float4>(qsrc + 4 * i);
+      __syncthreads();
+    }
+    // rows in sub-batches of SB: scores for every query head, then one
+    // online-softmax update per head and sub-batch.  The running max / sum
+    // belong to the lane's row group (LPR lanes sharing its rows), so no
+    // cross-lane maximum is needed inside the loop.
+#pragma unroll
+    for (int kb = 0; kb < KB; kb += SB) {
+      if (p0 + (kb * NW + wave) * RPW >= n) break;  // no row of this wave from here on
+      float sc[GM][SB];
+#pragma unroll
+      for (int j = 0; j < SB; ++j) {
+        const int k = kb + j;
+        const int r = p0 + (k * NW + wave) * RPW + sub;
+        float kf[EPL];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) kf[e] = row_elem<EPL>(kr[k], e);
 #pragma unroll
         for (int h = 0; h < GM; ++h) {
           if (h < G) {
-            const float p = sc[h * SC + r];
+            float d = 0.f;
 #pragma unroll
-            for (int e = 0; e < EPL; ++e) acc[h][e] = fmaf(p, row_elem<EPL>(vr[k], e), acc[h][e]);
+            for (int e = 0; e < EPL; e += 4) {
+              const float4 q4 = *reinterpret_cast<const float4*>(qs + h * HD + c * EPL + e);
+              d = fmaf(kf[e], q4.x, d); d = fmaf(kf[e + 1], q4.y, d);
+              d = fmaf(kf[e + 2], q4.z, d); d = fmaf(kf[e + 3], q4.w, d);
+            }
+            d = group_sum<LPR>(d) * m.attn_scale;
+            sc[h][j] = r < n ? d : -INFINITY;
+          }
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
+        if (h < G) {
+          float mx = sc[h][0];
+#pragma unroll
+          for (int j = 1; j < SB; ++j) mx = fmaxf(mx, sc[h][j]);
+          const float m_new = fmaxf(m_run[h], mx);
+          // a row group that has seen no row keeps (-inf, 0, 0)
+          const float mref = m_new == -INFINITY ? 0.f : m_new;
+          const float alpha = __expf(m_run[h] - mref);
+          float ls = 0.f;
+#pragma unroll
+          for (int j = 0; j < SB; ++j) {
+            sc[h][j] = __expf(sc[h][j] - mref);
+            ls += sc[h][j];
+          }
+          l_run[h] = l_run[h] * alpha + ls;
+          m_run[h] = m_new;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) acc[h][e] *= alpha;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < SB; ++j) {
+        float vf[EPL];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) vf[e] = row_elem<EPL>(vr[kb + j], e);
+#pragma unroll
+        for (int h = 0; h < GM; ++h) {
+          if (h < G) {
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[h][e] = fmaf(sc[h][j], vf[e], acc[h][e]);
           }
         }
       }
     }
-    __syncthreads();
   }
-  // reduce over the row groups of a wave (lanes with equal c), then over waves
+
+  // per wave: sum the accumulators of its row groups; then merge the waves
+  float* red = scr;                   // [NW][GM][HD]
+  float* stat = scr + NW * GM * HD;   // [NW][GM][2]
 #pragma unroll
   for (int h = 0; h < GM; ++h) {
     if (h < G) {
+      // merge the row groups of the wave: rescale each to the wave's max
+      float M = m_run[h];
+#pragma unroll
+      for (int o = LPR; o < 64; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+      const float f = m_run[h] == -INFINITY ? 0.f : __expf(m_run[h] - M);
+      float l = l_run[h] * f;
+#pragma unroll
+      for (int o = LPR; o < 64; o <<= 1) l += __shfl_xor(l, o);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
-        float v = acc[h][e];
+        float v = acc[h][e] * f;
 #pragma unroll
         for (int o = LPR; o < 64; o <<= 1) v += __shfl_xor(v, o);
         if (sub == 0) red[(wave * GM + h) * HD + c * EPL + e] = v;
+      }
+      if (lane == 0) {
+        stat[(wave * GM + h) * 2] = M;
+        stat[(wave * GM + h) * 2 + 1] = l;
       }
     }
   }
   __syncthreads();
   for (int i = threadIdx.x; i < G * HD; i += NT) {
     const int h = i / HD, d = i - h * HD;
-    float s = 0.f;
+    float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) s += red[(w * GM + h) * HD + d];
-    out[i] = s;
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, stat[(w * GM + h) * 2]);
+    float l = 0.f, o = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = stat[(w * GM + h) * 2];
+      if (mw != -INFINITY) {
+        const float f = __expf(mw - M);
+        l = fmaf(f, stat[(w * GM + h) * 2 + 1], l);
+        o = fmaf(f, red[(w * GM + h) * HD + d], o);
+      }
+    }
+    if (record) {
+      float* rec = dst + h * (kPartHead + HD);
+      stg<float>(rec + kPartHead + d, o);
+      if (d == 0) stg<float2>(rec, make_float2(M, l));
+    } else {
+      stg<float>(dst + h * HD + d, o / l);
+    }
   }
 }
 
@@ -848,31 +893,66 @@ __device__ __forceinline__ int active_splits(const DevModel& m, int pos, int* ch
   return (n_pos + chunk - 1) / chunk;
 }
 
-// Store this split's result: the normalised head outputs when it is the only
-// split with work, else the (m, l, unnormalised acc) record the combine reads.
+// Merge the S (> 1) split records of KV group g into the normalised output of
+// its query heads: o_h = sum_s exp(m_s - M) acc_s / sum_s exp(m_s - M) l_s.
+// All waves: first the per-(head, split) weights, then every thread sums a
+// float4 of the output over a share of the splits with all its loads in
+// flight, then the shares are added through LDS.
 template <int HD, int GM>
-__device__ __forceinline__ void epi_attn(const DevModel& m, const amk_task_t& t, const float* scr, const Ctl& ctl,
-                                         int pos, int lane) {
-  using A = AttnGeom<HD, GM>;
+__device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g, int S, float* scr, int wave,
+                                             int lane) {
   const int G = m.group;
-  int chunk;
-  const int active = active_splits(m, pos, &chunk);
-  if (t.begin >= active) return;  // empty split: nothing to publish
-  const float* out = scr + GM * A::SC + NW * GM * HD;
-  if (active == 1) {
-    float* o = m.o + (size_t)t.layer * m.nq * HD + (size_t)t.aux * G * HD;
-    for (int h = 0; h < G; ++h) {
-      const float inv = 1.0f / ctl.l_run[h];
-      for (int e = lane; e < HD; e += 64) stg<float>(o + h * HD + e, out[h * HD + e] * inv);
-    }
-    return;
-  }
   const int rec = G * (kPartHead + HD);
-  float* dst = m.part + ((size_t)(t.layer * m.nkv + t.aux) * m.nsplit + t.begin) * rec;
-  for (int h = 0; h < G; ++h) {
-    float* d = dst + h * (kPartHead + HD);
-    if (lane == 0) stg<float2>(d, make_float2(ctl.m_run[h], ctl.l_run[h]));
-    for (int e = lane; e < HD; e += 64) stg<float>(d + kPartHead + e, out[h * HD + e]);
+  const float* base = m.part + ((size_t)(layer * m.nkv + g) * m.nsplit) * rec;
+  float* wts = scr;                                        // [GM][64]
+  float4* red = reinterpret_cast<float4*>(scr + GM * 64);  // [SP][E4]
+  if (wave < G) {
+    const int h = wave;
+    float ms = -INFINITY, ls = 0.f;
+    if (lane < S) {
+      const float2 ml = ldg<float2>(base + (size_t)lane * rec + h * (kPartHead + HD));
+      ms = ml.x;
+      ls = ml.y;
+    }
+    const float M = wave_max(ms);
+    const float w = lane < S ? __expf(ms - M) : 0.f;
+    const float inv = 1.0f / wave_sum(w * ls);
+    wts[h * 64 + lane] = w * inv;
+  }
+  __syncthreads();
+  const int E4 = G * HD / 4;         // float4s of output
+  const int SP = max(1, NT / E4);    // split shares
+  const int t = threadIdx.x;
+  const int o4 = t % E4, sp = t / E4;
+  const int h = (4 * o4) / HD, d = 4 * o4 - h * HD;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (sp < SP) {
+    const float* src = base + h * (kPartHead + HD) + kPartHead + d;
+    for (int s0 = sp; s0 < S; s0 += 8 * SP) {
+      float4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int s = s0 + k * SP;
+        v[k] = s < S ? ldg<float4>(src + (size_t)s * rec) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int s = s0 + k * SP;
+        const float w = s < S ? wts[h * 64 + s] : 0.f;
+        a.x = fmaf(w, v[k].x, a.x); a.y = fmaf(w, v[k].y, a.y);
+        a.z = fmaf(w, v[k].z, a.z); a.w = fmaf(w, v[k].w, a.w);
+      }
+    }
+    red[sp * E4 + o4] = a;
+  }
+  __syncthreads();
+  if (t < E4) {
+    float4 o = red[t];
+    for (int k = 1; k < SP; ++k) {
+      const float4 v = red[k * E4 + t];
+      o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
+    }
+    stg<float4>(m.o + ((size_t)layer * m.nq + (size_t)g * G) * HD + 4 * t, o);
   }
 }
 
@@ -897,6 +977,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
   for (int i = threadIdx.x; i < m.lds_act; i += NT) L.act[i] = 0.f;
   if (threadIdx.x == 0) {
     ctl.abort = 0;
+    ctl.cont = 0;
     ctl.res_buf = -1;
     ctl.res_lo = ctl.res_hi = 0;
   }
@@ -910,6 +991,10 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
 
   auto prefetch = [&](int idx) {
     g0 = g1 = gi = 0;
+    // redefined on every path, so the buffers are dead between a consumer
+    // and the next prefetch (attention and inline tasks reuse the registers)
+#pragma unroll
+    for (int i = 0; i < PIPE; ++i) bufA[i] = bufB[i] = make_uint4(0, 0, 0, 0);
     if (idx >= qe) return;
     const amk_task_t tn = ldc<amk_task_t>(m.tasks + idx);
     if (!is_gemv(tn.op)) return;
@@ -948,12 +1033,17 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     __syncthreads();
     if (ctl.abort) return;
 
-    // an attention split with no positions at `pos` has no input and no work
-    const bool idle = t.op == AMK_OP_ATTN && t.begin >= active_splits(m, pos, nullptr);
+    // an attention split with no positions at `pos` has no work
+    const bool attn = t.op == AMK_OP_ATTN;
+    int chunk = 0;
+    const int active = attn ? active_splits(m, pos, &chunk) : 0;
+    const bool idle = attn && t.begin >= active;
 
     // ---- B1b: every wave moves its slice of the input activation
-    if (!idle) load_input(m, t, token, L, ctl, wave, lane);
-    __syncthreads();
+    if (gemv) {
+      load_input(m, t, token, L, ctl, wave, lane);
+      __syncthreads();
+    }
     if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());
 
     // ---- compute
@@ -972,18 +1062,22 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         const float s = wave_sum(acc);
         if (lane == 0) mypart[cj] = s;
       }
-    } else if (t.op == AMK_OP_ATTN && !idle) {
-      attention<HD, GM>(m, t, pos, kv, L.act, L.part, ctl, wave, lane);
+    } else if (attn && !idle) {
+      // one split: the normalised output directly; several: a partial record
+      const int j0 = t.begin * chunk, j1 = min(pos + 1, j0 + chunk);
+      const int rec = m.group * (kPartHead + HD);
+      float* dst = active == 1 ? m.o + ((size_t)t.layer * m.nq + (size_t)t.aux * m.group) * HD
+                               : m.part + (((size_t)t.layer * m.nkv + t.aux) * m.nsplit + t.begin) * rec;
+      attention<HD, GM>(m, t.layer, t.aux, j0, j1, kv, L.act, L.part, dst, active > 1, wave, lane);
+      drain_vmem();
     }
-    __syncthreads();  // B2: results in LDS
+    __syncthreads();  // B2: GEMV partials in LDS, attention results stored
 
-    // ---- publish (sync wave), then stream the next task (streaming waves)
+    // ---- publish (sync wave)
     if (wave == 0) {
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_COMPUTE_END, (uint64_t)wall_clock64());
       switch (t.op) {
         case AMK_OP_QKV: epi_qkv(m, t, g, L, pos, kv, input_rs(m, ctl), lane); break;
-        case AMK_OP_ATTN: epi_attn<HD, GM>(m, t, L.part, ctl, pos, lane); break;
-        case AMK_OP_COMBINE: combine_heads(m, t.layer, t.begin, t.end, pos, lane); break;
         case AMK_OP_O: case AMK_OP_DOWN: epi_residual(m, t, g, L, ctl, lane); break;
         case AMK_OP_GATEUP: epi_gateup(m, t, g, L, input_rs(m, ctl), lane); break;
         case AMK_OP_LMHEAD: epi_lmhead(m, t, g, L, input_rs(m, ctl), logits, lane); break;
@@ -991,21 +1085,41 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         default: break;
       }
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_PUBLISHED, (uint64_t)wall_clock64());
+      bool cont = false;
       if (t.chain_counter >= 0) {
-        // attention split: the last split of this KV head to finish runs the
-        // head's inline combine (its producers are the head's nsplit splits)
-        if (release_signal_last(m, t.signal_counter, epoch * (uint32_t)m.nsplit, lane)) {
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-          if (active_splits(m, pos, nullptr) > 1)
-            combine_heads(m, t.layer, t.aux * m.group, (t.aux + 1) * m.group, pos, lane);
-          release_signal(m, t.chain_counter, lane);
-        }
+        // the producer that completes the counter runs its inline task: a QKV
+        // task's group has npg producers, an attention split's nsplit
+        const uint32_t producers = t.op == AMK_OP_QKV ? (uint32_t)m.npg : (uint32_t)m.nsplit;
+        cont = release_signal_last(m, t.signal_counter, epoch * producers, lane);
+        if (cont) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       } else {
         release_signal(m, t.signal_counter, lane);
       }
+      if (lane == 0) ctl.cont = cont;
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SIGNALLED, (uint64_t)wall_clock64());
     }
     __syncthreads();  // B3: results released and signalled
+
+    // ---- inline task of the chain counter (all waves)
+    if (ctl.cont) {
+      if (t.op == AMK_OP_QKV) {
+        float* dst = m.o + ((size_t)t.layer * m.nq + (size_t)t.aux * m.group) * HD;
+        attention<HD, GM>(m, t.layer, t.aux, 0, pos + 1, kv, L.act, L.part, dst, false, wave, lane);
+      } else if (active > 1) {
+        merge_splits<HD, GM>(m, t.layer, t.aux, active, L.part, wave, lane);
+      }
+      drain_vmem();
+      __syncthreads();  // B4: inline results stored
+      if (wave == 0) {
+        release_signal(m, t.chain_counter, lane);
+        if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_CHAINED, (uint64_t)wall_clock64());
+      }
+      __syncthreads();  // B5: the next task's loads go out after the chain signal
+    } else if (tr && wave == 0 && lane == 0) {
+      stg<uint64_t>(tr + AMK_TRACE_CHAINED, 0ull);
+    }
+
+    // ---- the next task's static data (sync wave) and weight stream (streaming waves)
     if (wave == 0) {
       if (idx + 1 < qe) load_static(m, ldc<amk_task_t>(m.tasks + idx + 1), token, pos, L, ctl, lane);
     } else {
@@ -1028,11 +1142,12 @@ static const void* kernel_for(int head_dim, int group) {
 
 extern "C" int amk_internal_threads(void) { return NT; }
 
-// Floats of LDS scratch the attention of one task needs (in the partials region).
+// Floats of LDS scratch the attention and split merge of one task need (in
+// the partials region).
 extern "C" int amk_internal_attn_scratch(int group, int head_dim) {
   const bool small = group <= 4;
-  if (head_dim == 64) return small ? AttnGeom<64, 4>::SCRATCH : AttnGeom<64, 8>::SCRATCH;
-  return small ? AttnGeom<128, 4>::SCRATCH : AttnGeom<128, 8>::SCRATCH;
+  if (head_dim == 64) return small ? AttnGeom<64, 4>::LDS : AttnGeom<64, 8>::LDS;
+  return small ? AttnGeom<128, 4>::LDS : AttnGeom<128, 8>::LDS;
 }
 
 extern "C" int amk_internal_prepare(int head_dim, int group, int lds_bytes) {

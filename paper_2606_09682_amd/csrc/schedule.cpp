@@ -74,9 +74,39 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
   s->fmt = cfg->weight_format; s->tied = cfg->tied_embeddings;
   s->group = nq / nkv; s->half = hd / 2;
   s->units = (nq + 2 * nkv) * s->half; s->q_units = nq * s->half;
+  s->gunits = (s->group + 2) * s->half;
   s->nsplit = nsplit; s->max_jobs = max_jobs;
   s->theta = cfg->rope_theta; s->eps = cfg->rms_eps;
+  // QKV tasks per KV group: the grid's share of the whole QKV stage, at least
+  // one task per group and few enough units per task for the row cap
+  {
+    const int n_qkv = stage_tasks(s->units, 2, n_cu, max_jobs);
+    int npg = std::max(1, std::min(n_qkv / nkv, s->gunits));
+    while (((s->gunits + npg - 1) / npg) * 2 > max_jobs) ++npg;
+    s->npg = npg;
+  }
+  const int sc = tuning ? tuning->short_context : 0;
+  s->short_context = sc == 0 ? kDefaultShortContext : sc < 0 ? 0 : sc;
   return AMK_OK;
+}
+
+int stage_tasks(int items, int jobs_per_item, int n_cu, int max_jobs) {
+  int n = std::min(n_cu, items);
+  const int need = (int)(((long)items * jobs_per_item + max_jobs - 1) / max_jobs);
+  // each task must also hold whole items: ceil(items / n) * jobs_per_item <= max_jobs
+  n = std::max(n, need);
+  while (((items + n - 1) / n) * jobs_per_item > max_jobs) ++n;
+  return std::min(n, items);
+}
+
+UnitHead unit_head(const Shape& s, int u) {
+  const int slot = u / s.half;
+  const int g = slot / (s.group + 2), r = slot % (s.group + 2);
+  UnitHead h;
+  h.i = u % s.half;
+  if (r < s.group) { h.kind = 0; h.head = g * s.group + r; }
+  else { h.kind = r == s.group ? 1 : 2; h.head = g; }
+  return h;
 }
 
 int task_jobs(const Shape& s, const amk_task_t& t) {
@@ -92,7 +122,7 @@ int task_jobs(const Shape& s, const amk_task_t& t) {
 // ---------------------------------------------------------------------------
 // lowering
 // ---------------------------------------------------------------------------
-Schedule build_schedule(const Shape& s, int n_cu) {
+Schedule build_schedule(const Shape& s, int n_cu, int variant) {
   Schedule sch;
   std::vector<int> qlen(n_cu, 0);
   int n_ctr = 0;
@@ -115,14 +145,7 @@ Schedule build_schedule(const Shape& s, int n_cu) {
     sch.tasks.push_back(t);
   };
   // number of tasks for a stage of `items` work items of `jobs_per_item` rows
-  auto n_tasks = [&](int items, int jobs_per_item) {
-    int n = std::min(n_cu, items);
-    int need = (int)(((long)items * jobs_per_item + s.max_jobs - 1) / s.max_jobs);
-    // each task must also hold whole items: ceil(items / n) * jobs_per_item <= max_jobs
-    n = std::max(n, need);
-    while (((items + n - 1) / n) * jobs_per_item > s.max_jobs) ++n;
-    return std::min(n, items);
-  };
+  auto n_tasks = [&](int items, int jobs_per_item) { return stage_tasks(items, jobs_per_item, n_cu, s.max_jobs); };
   auto cu_of = [&](int i, int n) { return n >= n_cu ? i % n_cu : (rot + i) % n_cu; };
   auto bump = [&](int n) { if (n < n_cu) rot = (rot + n) % n_cu; };
   auto lo = [](int total, int parts, int i) { return (int)((long)total * i / parts); };
@@ -139,24 +162,44 @@ Schedule build_schedule(const Shape& s, int n_cu) {
     return std::make_pair(sig, n);
   };
 
+  const bool shortv = variant == AMK_SCHEDULE_SHORT;
   int prev_c = -1, prev_n = 0;  // counter of the stage producing the layer input
   for (int l = 0; l < s.L; ++l) {
-    auto qkv = stage(AMK_OP_QKV, l, s.units, 2, prev_c, prev_n);
-    // attention: one task per (KV head, position split).  The splits of a KV
-    // head signal that head's counter; the split that increments it last
-    // runs the head's inline COMBINE, which signals c_done.
-    const int c_done = n_ctr++;
-    const int c_grp0 = n_ctr;
+    // QKV: npg tasks per KV group over that group's units; each group's tasks
+    // signal the group's counter.
+    const int c_qkv0 = n_ctr;
     n_ctr += s.nkv;
-    const int n_attn = s.nkv * s.nsplit;
-    for (int i = 0; i < n_attn; ++i) {
-      const int g = i / s.nsplit;
-      add(AMK_OP_ATTN, l, cu_of(i, n_attn), i % s.nsplit, s.nsplit, g, {{qkv.first, qkv.second}}, c_grp0 + g,
-          c_done);
+    const int c_done = n_ctr++;  // every KV group's attention output is written
+    const int n_qkv = s.nkv * s.npg;
+    for (int g = 0; g < s.nkv; ++g) {
+      for (int i = 0; i < s.npg; ++i) {
+        std::vector<std::pair<int, int>> w;
+        if (prev_c >= 0) w.push_back({prev_c, prev_n});
+        const int b = g * s.gunits + lo(s.gunits, s.npg, i), e = g * s.gunits + lo(s.gunits, s.npg, i + 1);
+        add(AMK_OP_QKV, l, cu_of(g * s.npg + i, n_qkv), b, e, g, w, c_qkv0 + g, shortv ? c_done : -1);
+      }
     }
-    bump(n_attn);
-    for (int g = 0; g < s.nkv; ++g)
-      add(AMK_OP_COMBINE, l, AMK_CU_INLINE, g * s.group, (g + 1) * s.group, g, {{c_grp0 + g, s.nsplit}}, c_done);
+    bump(n_qkv);
+    if (shortv) {
+      // the QKV task of group g that finishes last runs the group's attention
+      for (int g = 0; g < s.nkv; ++g)
+        add(AMK_OP_ATTN, l, AMK_CU_INLINE, 0, 1, g, {{c_qkv0 + g, s.npg}}, c_done);
+    } else {
+      // one task per (KV group, position split); the splits of a group signal
+      // the group's counter, and the split that increments it last runs the
+      // group's inline COMBINE, which signals c_done
+      const int c_grp0 = n_ctr;
+      n_ctr += s.nkv;
+      const int n_attn = s.nkv * s.nsplit;
+      for (int i = 0; i < n_attn; ++i) {
+        const int g = i / s.nsplit;
+        add(AMK_OP_ATTN, l, cu_of(i, n_attn), i % s.nsplit, s.nsplit, g, {{c_qkv0 + g, s.npg}}, c_grp0 + g,
+            c_done);
+      }
+      bump(n_attn);
+      for (int g = 0; g < s.nkv; ++g)
+        add(AMK_OP_COMBINE, l, AMK_CU_INLINE, g * s.group, (g + 1) * s.group, g, {{c_grp0 + g, s.nsplit}}, c_done);
+    }
     auto o = stage(AMK_OP_O, l, s.H, 1, c_done, s.nkv);
     auto gu = stage(AMK_OP_GATEUP, l, s.I, 2, o.first, o.second);
     auto dn = stage(AMK_OP_DOWN, l, s.H, 1, gu.first, gu.second);
@@ -223,6 +266,7 @@ struct BufIds {
   int next() const { return 7 * L + 3; }
   int count() const { return 7 * L + 4; }
   bool is_kv(int b) const { return b >= 3 * L + 1 && b < 4 * L + 1; }
+  bool is_part(int b) const { return b >= 4 * L + 1 && b < 5 * L + 1; }
 };
 
 void accesses(const Shape& s, const BufIds& ids, const amk_task_t& t, std::vector<Access>* rd,
@@ -232,10 +276,18 @@ void accesses(const Shape& s, const BufIds& ids, const amk_task_t& t, std::vecto
   switch (t.op) {
     case AMK_OP_QKV: {
       rd->push_back({ids.x(2 * l), 0, s.H});
-      const int qb = std::min(t.end, s.q_units);
-      if (t.begin < qb) wr->push_back({ids.q(l), t.begin, qb});
-      const int kb = std::max(t.begin, s.q_units);
-      if (kb < t.end) wr->push_back({ids.kv(l), kb - s.q_units, t.end - s.q_units});
+      // group-major units -> query units (head-major) and K/V units (K heads, then V heads)
+      for (int g = t.begin / s.gunits; g * s.gunits < t.end; ++g) {
+        const int b = std::max(t.begin, g * s.gunits) - g * s.gunits;
+        const int e = std::min(t.end, (g + 1) * s.gunits) - g * s.gunits;
+        const int qn = s.group * s.half;
+        if (b < qn) wr->push_back({ids.q(l), g * qn + b, g * qn + std::min(e, qn)});
+        const int kb = std::max(b, qn), ke = std::min(e, qn + s.half);
+        if (kb < ke) wr->push_back({ids.kv(l), g * s.half + kb - qn, g * s.half + ke - qn});
+        const int vb = std::max(b, qn + s.half), ve = e;
+        if (vb < ve)
+          wr->push_back({ids.kv(l), (s.nkv + g) * s.half + vb - qn - s.half, (s.nkv + g) * s.half + ve - qn - s.half});
+      }
       break;
     }
     case AMK_OP_ATTN: {
@@ -243,7 +295,10 @@ void accesses(const Shape& s, const BufIds& ids, const amk_task_t& t, std::vecto
       rd->push_back({ids.kv(l), g * s.half, (g + 1) * s.half});                         // K head g
       rd->push_back({ids.kv(l), (s.nkv + g) * s.half, (s.nkv + g + 1) * s.half});       // V head g
       rd->push_back({ids.q(l), g * s.group * s.half, (g + 1) * s.group * s.half});
-      wr->push_back({ids.part(l), g * s.nsplit + t.begin, g * s.nsplit + t.begin + 1});
+      if (t.cu == AMK_CU_INLINE)  // the whole position range: writes the group's output
+        wr->push_back({ids.o(l), g * s.group * s.hd, (g + 1) * s.group * s.hd});
+      else
+        wr->push_back({ids.part(l), g * s.nsplit + t.begin, g * s.nsplit + t.begin + 1});
       break;
     }
     case AMK_OP_COMBINE: {
@@ -311,8 +366,8 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     const bool inl = t.cu == AMK_CU_INLINE;
     if (!inl && (t.cu < 0 || t.cu >= n_cu))
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: queue %ld out of range", i, t.cu);
-    if (inl && (t.op != AMK_OP_COMBINE || t.seq != 0))
-      return R.fail(AMK_CHECK_INLINE, i, -1, "task %ld: only a COMBINE (seq 0) may run inline", i);
+    if (inl && ((t.op != AMK_OP_COMBINE && t.op != AMK_OP_ATTN) || t.seq != 0))
+      return R.fail(AMK_CHECK_INLINE, i, -1, "task %ld: only an ATTN or COMBINE (seq 0) may run inline", i);
     if (t.chain_counter < -1 || t.chain_counter >= n_counters)
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: chain counter %ld out of range", i, t.chain_counter);
     const bool layered = t.op <= AMK_OP_DOWN;
@@ -338,11 +393,15 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
       case AMK_OP_ARGMAX: lim = n_lm; break;
     }
     if (t.op == AMK_OP_ATTN) {
-      if (t.end != s.nsplit || t.begin < 0 || t.begin >= s.nsplit || t.aux < 0 || t.aux >= s.nkv)
+      const bool split_ok = inl ? (t.begin == 0 && t.end == 1) : (t.end == s.nsplit && t.begin >= 0 && t.begin < s.nsplit);
+      if (!split_ok || t.aux < 0 || t.aux >= s.nkv)
         return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: bad attention split/head", i);
     } else if (t.begin < 0 || t.end > lim || t.begin >= t.end) {
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: range [%ld, ...) out of bounds", i, t.begin);
     }
+    if (t.op == AMK_OP_QKV && (t.aux < 0 || t.aux >= s.nkv || t.begin / s.gunits != t.aux ||
+                               (t.end - 1) / s.gunits != t.aux))
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: QKV units must lie in KV group aux %ld", i, t.aux);
     if (t.op == AMK_OP_ARGMAX && (t.begin != 0 || t.end != n_lm))
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: argmax must reduce all %ld partial slots", i, n_lm);
     if (t.op == AMK_OP_LMHEAD && (t.aux < 0 || t.aux >= n_lm))
@@ -410,6 +469,19 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     if (k < 0 || tasks[k].signal_counter != t.chain_counter)
       return R.fail(AMK_CHECK_INLINE, i, k, "task %ld chains to counter %ld without a matching inline task", i,
                     t.chain_counter);
+    // the device runs the continuation from the chaining task alone: a QKV
+    // task runs its group's attention, an attention split its group's
+    // combine, and it counts npg resp. nsplit producers on the way
+    const amk_task_t& it = tasks[k];
+    const bool pair_ok = (t.op == AMK_OP_QKV && it.op == AMK_OP_ATTN) ||
+                         (t.op == AMK_OP_ATTN && t.cu != AMK_CU_INLINE && it.op == AMK_OP_COMBINE);
+    if (!pair_ok || it.aux != t.aux || (it.op == AMK_OP_COMBINE && (it.begin != t.aux * s.group ||
+                                                                    it.end != (t.aux + 1) * s.group)))
+      return R.fail(AMK_CHECK_INLINE, i, k, "task %ld (op %ld) cannot run inline task %ld", i, t.op, k);
+    const int expect = t.op == AMK_OP_QKV ? s.npg : s.nsplit;
+    if ((int)producers[t.signal_counter].size() != expect)
+      return R.fail(AMK_CHECK_INLINE, i, t.signal_counter, "chained counter %ld has %ld producers, device counts %ld",
+                    t.signal_counter, (long)producers[t.signal_counter].size(), expect);
   }
 
   // ---- 3. queue order: a producer on the same CU must be queued earlier ------
@@ -506,13 +578,21 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     accesses(s, ids, tasks[i], &rd, &wr);
     for (auto& a : wr) writers[a.buf].push_back({a.lo, a.hi, i});
   }
-  // exactly-once outputs: writer intervals of each written buffer tile it
+  // exactly-once outputs: writer intervals of each written buffer tile it.
+  // Attention partials are scratch of the split schedule: required only
+  // where some task reads them.
+  std::vector<char> read_any(nb, 0);
+  for (int i = 0; i < n; ++i) {
+    accesses(s, ids, tasks[i], &rd, &wr);
+    for (auto& a : rd) read_any[a.buf] = 1;
+  }
   for (int b = 0; b < nb; ++b) {
     auto& v = writers[b];
     if (b == ids.x(0)) {
       if (!v.empty()) return R.fail(AMK_CHECK_OUTPUT, v[0].task, -1, "task %ld writes the embedding input", v[0].task);
       continue;
     }
+    if (ids.is_part(b) && v.empty() && !read_any[b]) continue;
     std::sort(v.begin(), v.end(), [](const W& a, const W& c) { return a.lo < c.lo; });
     int at = 0;
     for (auto& w : v) {

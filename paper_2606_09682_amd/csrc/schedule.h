@@ -23,11 +23,18 @@ struct Shape {
   int group = 0;         // query heads per KV head
   int half = 0;          // hd / 2: RoPE row pairs per head
   int units = 0;         // (nq + 2 nkv) * half: q/k/v row-pair units
+  int gunits = 0;        // (group + 2) * half: units of one KV group
   int q_units = 0;       // nq * half
-  int nsplit = 0;        // attention position splits per KV head
+  int npg = 0;           // QKV tasks per KV group
+  int nsplit = 0;        // attention position splits per KV head (long schedule)
   int max_jobs = 0;      // GEMV rows per task cap
+  int short_context = 0; // steps with pos + 1 <= short_context use the short schedule
   float theta = 0.f, eps = 0.f;
 };
+
+// Number of tasks of a GEMV stage over `items` items of `jobs_per_item` rows:
+// one per CU (at most one per item), more if the row cap requires.
+int stage_tasks(int items, int jobs_per_item, int n_cu, int max_jobs);
 
 // Validates the config (shape family, divisibility, 16-byte row alignment)
 // and fills *s.  Returns AMK_OK or AMK_ERR_INVALID_ARGUMENT / _UNSUPPORTED
@@ -42,8 +49,19 @@ struct Schedule {
   int n_lm_slots = 0;              // argmax partial slots (one per LM-head task)
 };
 
-// Deterministic lowering of one decode step onto n_cu queues.
-Schedule build_schedule(const Shape& s, int n_cu);
+// Default of amk_tuning_t.short_context.
+constexpr int kDefaultShortContext = 256;
+
+// Deterministic lowering of one decode step onto n_cu queues, schedule
+// variant AMK_SCHEDULE_SHORT or AMK_SCHEDULE_LONG.
+Schedule build_schedule(const Shape& s, int n_cu, int variant);
+
+// Which head a QKV unit belongs to: kind 0 = query head `head`, 1 = K head,
+// 2 = V head (head = KV group); i = row-pair index within the head.
+struct UnitHead {
+  int kind, head, i;
+};
+UnitHead unit_head(const Shape& s, int u);
 
 // Static check (never throws).  Fills *rep; returns true iff accepted.
 bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n_tasks,

@@ -24,6 +24,16 @@ pytestmark = pytest.mark.gpu
 
 TOL = 2e-2
 
+# amk_tuning_t.short_context values forcing one schedule variant
+SHORT_ALWAYS = 1 << 30
+LONG_ALWAYS = -1
+
+
+def tuning_for(amk, variant=None, **kw):
+    sc = {None: 0, "short": SHORT_ALWAYS, "long": LONG_ALWAYS}[variant]
+    return amk.amk_tuning_t(kw.get("attn_splits", 0), kw.get("timeout_us", 0), kw.get("max_rows", 0),
+                            kw.get("trace", 0), sc)
+
 
 def say(msg):
     print(f"[gpu-test] {msg}", file=sys.stderr, flush=True)
@@ -63,7 +73,8 @@ def weights_for(name, seed=0):
 
 def gpu_decode(amk, torch, w, fmt, pos0, steps, kv_np, max_seq, tuning=None):
     cfg = w.cfg
-    say(f"{cfg.name} {fmt} pos0={pos0} steps={steps} max_seq={max_seq}")
+    sc = tuning.short_context if tuning is not None else 0
+    say(f"{cfg.name} {fmt} pos0={pos0} steps={steps} max_seq={max_seq} short_context={sc}")
     dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, fmt, max_seq)), weights_to_device(w, fmt), tuning)
     kv = kv_to_device(kv_np)
     logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
@@ -125,16 +136,19 @@ def test_tiny_greedy(amk, torch_cuda, fmt):
     compare("tiny", fmt, g, o, 0)
 
 
+@pytest.mark.parametrize("variant", ["short", "long"])
 @pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
-@pytest.mark.parametrize("pos", [1, 63, 64, 65, 300, 1000])
-def test_tiny_filled_cache(amk, torch_cuda, fmt, pos):
-    """Single steps over a cache filled with N(0,1) rows: split boundaries and ragged chunks."""
+@pytest.mark.parametrize("pos", [1, 63, 64, 65, 300, 575, 576, 577, 1000])
+def test_tiny_filled_cache(amk, torch_cuda, fmt, pos, variant):
+    """Single steps over a cache filled with N(0,1) rows under both schedule
+    variants: split boundaries, ragged chunks, and whole-range inline
+    attention past one pass of the workgroup (576 rows at head_dim 64)."""
     w = weights_for("tiny")
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=1024 + 8)
-    g = gpu_decode(amk, torch_cuda, w, fmt, pos, 2, kv, kv.shape[3])
+    g = gpu_decode(amk, torch_cuda, w, fmt, pos, 2, kv, kv.shape[3], tuning=tuning_for(amk, variant))
     o = oracle_decode(w, fmt, pos, 2, kv)
-    compare("tiny", fmt, g, o, pos)
+    compare(f"tiny {variant}", fmt, g, o, pos)
 
 
 @pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
@@ -145,7 +159,7 @@ def test_tiny_attention_split_counts(amk, torch_cuda, fmt):
     kv = synth.make_kv_cache(cfg, 200, seed=1, max_seq=256)
     o = oracle_decode(w, fmt, 200, 1, kv)
     for splits in (1, 3, 64):
-        t = amk.amk_tuning_t(splits, 0, 0)
+        t = tuning_for(amk, "long", attn_splits=splits)
         g = gpu_decode(amk, torch_cuda, w, fmt, 200, 1, kv, kv.shape[3], tuning=t)
         compare(f"tiny splits={splits}", fmt, g, o, 200)
 
@@ -158,8 +172,10 @@ def test_tiny_small_tasks(amk, torch_cuda, fmt):
     kv = synth.make_kv_cache(cfg, 0)
     o = oracle_decode(w, fmt, 0, 3, kv)
     for cap in (2, 6):
-        g = gpu_decode(amk, torch_cuda, w, fmt, 0, 3, kv, cfg.seq_capacity, tuning=amk.amk_tuning_t(0, 0, cap))
-        compare(f"tiny rows/task={cap}", fmt, g, o, 0)
+        for variant in ("short", "long"):
+            g = gpu_decode(amk, torch_cuda, w, fmt, 0, 3, kv, cfg.seq_capacity,
+                           tuning=tuning_for(amk, variant, max_rows=cap))
+            compare(f"tiny rows/task={cap} {variant}", fmt, g, o, 0)
 
 
 @pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
@@ -175,25 +191,66 @@ def test_smollm2_greedy(amk, torch_cuda, fmt):
 @pytest.mark.parametrize("name", ["tinyllama_1b", "llama32_1b"])
 @pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
 def test_1b_positions(amk, torch_cuda, name, fmt):
+    """Each position under the variant the step selects by default and under
+    the other one."""
     w = weights_for(name)
     cfg = w.cfg
     for pos in cfg.positions:
         kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=pos + 2)
-        g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3])
         o = oracle_decode(w, fmt, pos, 1, kv)
-        compare(name, fmt, g, o, pos)
+        for variant in (None, "long" if pos + 1 <= 256 else "short"):
+            g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3], tuning=tuning_for(amk, variant))
+            compare(f"{name} {variant or 'default'}", fmt, g, o, pos)
 
 
 @pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
 def test_8b_positions(amk, torch_cuda, fmt):
-    """Full-size Llama-3-8B shape at positions 0 and 8192: every logit checked."""
+    """Full-size Llama-3-8B shape at positions 0 and 8192 under both schedule
+    variants: every logit checked."""
     w = weights_for("llama3_8b")
     cfg = w.cfg
     for pos in cfg.positions:
         kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=pos + 2)
-        g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3])
         o = oracle_decode(w, fmt, pos, 1, kv)
-        compare("llama3_8b", fmt, g, o, pos)
+        for variant in ("short", "long"):
+            g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3], tuning=tuning_for(amk, variant))
+            compare(f"llama3_8b {variant}", fmt, g, o, pos)
+
+
+@pytest.mark.parametrize("variant", ["short", "long"])
+def test_trace_records(amk, torch_cuda, variant):
+    """Per-task device timestamps are ordered within each task, every task
+    ran, and exactly one task per (layer, KV group) ran its inline task."""
+    import torch
+    w = weights_for("tiny")
+    cfg = w.cfg
+    pos = 100
+    kv_np = synth.make_kv_cache(cfg, pos, seed=1, max_seq=256)
+    tuning = tuning_for(amk, variant, trace=1)
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", 256)), weights_to_device(w, "bf16"), tuning)
+    kv = kv_to_device(kv_np)
+    logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+    dec.step(1, pos, kv, logits)
+    want = amk.AMK_SCHEDULE_SHORT if variant == "short" else amk.AMK_SCHEDULE_LONG
+    tasks, _ = amk.amk_schedule_export(dec.cfg, torch.cuda.get_device_properties(0).multi_processor_count,
+                                       tuning, variant=want)
+    got, tr = amk.amk_trace_copy(dec.handle, len(tasks))
+    assert dec.status() == amk.AMK_OK
+    dec.close()
+    assert got == want and len(tr) == len(tasks)
+    chained = {}
+    for t, r in zip(tasks, tr):
+        if t.cu == amk.AMK_CU_INLINE:
+            continue
+        assert 0 < r[amk.AMK_TRACE_WAIT_BEGIN] <= r[amk.AMK_TRACE_WAIT_END] <= r[amk.AMK_TRACE_COMPUTE_END]
+        assert r[amk.AMK_TRACE_COMPUTE_END] <= r[amk.AMK_TRACE_PUBLISHED] <= r[amk.AMK_TRACE_SIGNALLED]
+        if r[amk.AMK_TRACE_CHAINED]:
+            assert t.chain_counter >= 0 and r[amk.AMK_TRACE_CHAINED] >= r[amk.AMK_TRACE_SIGNALLED]
+            key = (t.layer, t.aux)
+            assert key not in chained
+            chained[key] = t.op
+    assert sorted(chained) == [(l, g) for l in range(cfg.n_layers) for g in range(cfg.n_kv_heads)]
+    assert set(chained.values()) == {amk.AMK_OP_QKV if variant == "short" else amk.AMK_OP_ATTN}
 
 
 def test_invalid_arguments(amk, torch_cuda):
@@ -222,7 +279,7 @@ def test_forced_timeout_is_sticky_and_recoverable(amk, torch_cuda):
     kv_np = synth.make_kv_cache(cfg, 0)
     say("tiny forced timeout (timeout_us=1)")
     dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", cfg.seq_capacity)), weights_to_device(w, "bf16"),
-                      amk.amk_tuning_t(0, 1, 0))
+                      tuning_for(amk, None, timeout_us=1))
     kv = kv_to_device(kv_np)
     logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
     dec.step(1, 0, kv, logits)

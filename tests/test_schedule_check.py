@@ -59,16 +59,17 @@ def producers(tasks, c):
 
 @pytest.mark.parametrize("name", list(synth.CONFIGS))
 @pytest.mark.parametrize("n_cu", [256, 13])
-def test_real_lowering_accepted(lib, name, n_cu):
+@pytest.mark.parametrize("variant", [amk.AMK_SCHEDULE_SHORT, amk.AMK_SCHEDULE_LONG])
+def test_real_lowering_accepted(lib, name, n_cu, variant):
     cfg = cfg_of(name, "w8a16")
-    tasks, nc = amk.amk_schedule_export(cfg, n_cu)
+    tasks, nc = amk.amk_schedule_export(cfg, n_cu, variant=variant)
     rep = check(cfg, tasks, nc, n_cu)
     assert rep.ok == 1, rep.message
     # one queue per CU, every queue used, seq contiguous; inline tasks sit on no queue
     seen = {}
     for t in tasks:
         if t.cu == amk.AMK_CU_INLINE:
-            assert t.op == amk.AMK_OP_COMBINE
+            assert t.op == (amk.AMK_OP_ATTN if variant == amk.AMK_SCHEDULE_SHORT else amk.AMK_OP_COMBINE)
             continue
         seen.setdefault(t.cu, []).append(t.seq)
     assert sorted(seen) == list(range(n_cu))
@@ -92,8 +93,41 @@ def test_schedule_shape_8b(lib):
     comb = [t for t in tasks if t.op == amk.AMK_OP_COMBINE]
     assert len(comb) == 8 * L and all(t.cu == amk.AMK_CU_INLINE for t in comb)
     assert all(t.wait_count[0] == 32 for t in comb)
-    # every QKV task owns whole RoPE row pairs: 48 heads * 64 pairs / 256 = 12 units each
-    assert {t.end - t.begin for t in tasks if t.op == amk.AMK_OP_QKV} == {12}
+    # every QKV task owns whole RoPE row pairs: 48 heads * 64 pairs / 256 = 12 units each,
+    # 32 tasks per KV group of (4 + 2) heads * 64 pairs
+    qkv = [t for t in tasks if t.op == amk.AMK_OP_QKV]
+    assert {t.end - t.begin for t in qkv} == {12}
+    assert all(t.begin // 384 == t.aux == (t.end - 1) // 384 for t in qkv)
+    assert all(t.chain_counter == -1 for t in qkv)
+
+
+def test_schedule_shape_8b_short(lib):
+    cfg = cfg_of("llama3_8b")
+    tasks, nc = amk.amk_schedule_export(cfg, 256, variant=amk.AMK_SCHEDULE_SHORT)
+    assert check(cfg, tasks, nc, 256).ok
+    L = 32
+    queued_attn = [t for t in tasks if t.op == amk.AMK_OP_ATTN and t.cu != amk.AMK_CU_INLINE]
+    inline_attn = [t for t in tasks if t.op == amk.AMK_OP_ATTN and t.cu == amk.AMK_CU_INLINE]
+    assert not queued_attn and not [t for t in tasks if t.op == amk.AMK_OP_COMBINE]
+    assert len(inline_attn) == 8 * L
+    assert all(t.wait_count[0] == 32 and (t.begin, t.end) == (0, 1) for t in inline_attn)
+    # each QKV task chains to its layer's attention-output counter, which O waits on
+    qkv = [t for t in tasks if t.op == amk.AMK_OP_QKV]
+    assert len(qkv) == 256 * L
+    for t in qkv:
+        assert t.chain_counter >= 0
+        group_inline = [a for a in inline_attn if a.layer == t.layer and a.aux == t.aux]
+        assert len(group_inline) == 1 and group_inline[0].signal_counter == t.chain_counter
+        assert group_inline[0].wait_counter[0] == t.signal_counter
+    o = [t for t in tasks if t.op == amk.AMK_OP_O and t.layer == 5]
+    assert {t.wait_counter[0] for t in o} == {a.signal_counter for a in inline_attn if a.layer == 5}
+    assert all(t.wait_count[0] == 8 for t in o)
+    # one queue per CU: four GEMV tasks per layer on every CU, nothing else
+    per_cu = {}
+    for t in tasks:
+        if t.cu != amk.AMK_CU_INLINE and t.op in (amk.AMK_OP_QKV, amk.AMK_OP_O, amk.AMK_OP_GATEUP, amk.AMK_OP_DOWN):
+            per_cu[t.cu] = per_cu.get(t.cu, 0) + 1
+    assert set(per_cu.values()) == {4 * L}
 
 
 # ------------------------------------------------------------------ mutants
@@ -306,3 +340,72 @@ def test_o_reading_before_combine_rejected(tiny_sched):
     m[i].wait_count[0] = m[comb].wait_count[0]
     rep = check(cfg, m, nc)
     assert not rep.ok and rep.rule in (amk.AMK_CHECK_RACE, amk.AMK_CHECK_INLINE), rep.message
+
+
+# ------------------------------------------------------------------ short schedule (inline attention)
+@pytest.fixture(scope="module")
+def tiny_short(lib):
+    cfg = cfg_of("tiny")
+    tasks, nc = amk.amk_schedule_export(cfg, N_CU, variant=amk.AMK_SCHEDULE_SHORT)
+    assert check(cfg, tasks, nc).ok
+    return cfg, tasks, nc
+
+
+def test_short_qkv_without_chain_rejected(tiny_short):
+    cfg, tasks, nc = tiny_short
+    m = clone(tasks)
+    m[find(m, amk.AMK_OP_QKV, 1)].chain_counter = -1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_INLINE, rep.message
+
+
+def test_short_inline_attention_of_other_group_rejected(tiny_short):
+    """The device runs the chaining task's own group: an inline attention
+    labelled with another group does not pair up."""
+    cfg, tasks, nc = tiny_short
+    m = clone(tasks)
+    i = find(m, amk.AMK_OP_ATTN, 2, lambda t: t.aux == 0)
+    m[i].aux = 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule in (amk.AMK_CHECK_INLINE, amk.AMK_CHECK_OUTPUT), rep.message
+
+
+def test_short_qkv_task_across_groups_rejected(tiny_short):
+    cfg, tasks, nc = tiny_short
+    m = clone(tasks)
+    # widen the last task of group 0 into group 1 and shrink its neighbour
+    i = find(m, amk.AMK_OP_QKV, 0, lambda t: t.aux == 0 and t.end % 128 == 0 and t.end > 0)
+    j = find(m, amk.AMK_OP_QKV, 0, lambda t: t.begin == m[i].end)
+    m[i].end += 1
+    m[j].begin += 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_WELL_FORMED, rep.message
+
+
+def test_short_o_waiting_on_qkv_counter_rejected(tiny_short):
+    """O waiting on one group's QKV counter instead of the attention output:
+    it would read attention outputs nobody has ordered before it."""
+    cfg, tasks, nc = tiny_short
+    m = clone(tasks)
+    a = find(m, amk.AMK_OP_ATTN, 1)
+    i = find(m, amk.AMK_OP_O, 1)
+    m[i].wait_counter[0] = m[a].wait_counter[0]
+    m[i].wait_count[0] = m[a].wait_count[0]
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_RACE, rep.message
+
+
+def test_short_producer_count_mismatch_rejected(tiny_short):
+    """A QKV task of group 1 relabelled to signal group 0's counter: every
+    wait count is fixed up to stay an all-join, but the chaining tasks of
+    group 0 would count one producer more than the device expects."""
+    cfg, tasks, nc = tiny_short
+    m = clone(tasks)
+    g0 = find(m, amk.AMK_OP_ATTN, 0, lambda t: t.aux == 0)
+    g1 = find(m, amk.AMK_OP_ATTN, 0, lambda t: t.aux == 1)
+    i = find(m, amk.AMK_OP_QKV, 0, lambda t: t.aux == 1)
+    m[i].signal_counter = m[g0].wait_counter[0]
+    m[g0].wait_count[0] += 1
+    m[g1].wait_count[0] -= 1
+    rep = check(cfg, m, nc)
+    assert not rep.ok, rep.message
