@@ -35,8 +35,12 @@
 // Llama-3-8B shape, deeper pipelines both delay the sync wave's polls and
 // input loads and stream no faster.
 //
-// Only the sync wave executes agent-scope acquire/release sequences: their
-// vmcnt(0) drains would otherwise stall the streaming waves' in-flight loads.
+// Every result another workgroup reads is stored coherent at agent scope
+// (write-through past the XCD's L2), so releasing it takes only a drain of
+// the storing wave's own stores before the counter increment: no L2
+// writeback.  Only the sync wave waits on counters (acquire: invalidate,
+// then plain loads) and increments them; streaming waves never drain while
+// their weight loads are in flight.
 // Lane reductions use DPP (VALU latency) rather than LDS permutes.
 //
 // No MFMA: a batch-1 GEMV is a matrix-vector product, bound by HBM bandwidth.
@@ -88,6 +92,23 @@ __device__ __forceinline__ void stg(void* p, const T& v) {
   using B = typename Bits<sizeof(T)>::T;
   *(AMK_GLOBAL B*)p = __builtin_bit_cast(B, v);
 }
+// Store of a published result: coherent at agent scope (written through the
+// XCD's L2), so a producer releases its results by draining its stores
+// (s_waitcnt vmcnt(0)) before the counter increment, with no L2 writeback.
+__device__ __forceinline__ void stc(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void stc(uint16_t* p, uint16_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void stc(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void stc(float2* p, float2 v) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), __builtin_bit_cast(uint64_t, v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <typename T>
 __device__ __forceinline__ T ldc(const void* p) {
   using B = typename Bits<sizeof(T)>::T;
@@ -381,7 +402,7 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
 }
 
 __device__ __forceinline__ void release_signal(const DevModel& m, int counter, int lane) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  drain_vmem();  // every published store of this wave is coherent at agent scope
   if (lane == 0 && counter >= 0)
     __hip_atomic_fetch_add(m.counters + (size_t)counter * kCounterStride, 1u, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
@@ -391,7 +412,7 @@ __device__ __forceinline__ void release_signal(const DevModel& m, int counter, i
 // to `target` (the last producer of this launch).  The caller that gets true
 // acquires before reading what the other producers released.
 __device__ __forceinline__ bool release_signal_last(const DevModel& m, int counter, uint32_t target, int lane) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  drain_vmem();
   uint32_t old = 0;
   if (lane == 0)
     old = __hip_atomic_fetch_add(m.counters + (size_t)counter * kCounterStride, 1u, __ATOMIC_RELAXED,
@@ -578,13 +599,13 @@ __device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, 
     }
     if (mat == W_Q) {
       float* qd = m.q + (size_t)l * m.nq * m.hd + (size_t)head * m.hd;
-      stg<float>(qd + i, y0);
-      stg<float>(qd + i + m.half, y1);
+      stc(qd + i, y0);
+      stc(qd + i + m.half, y1);
     } else {
       const int which = (mat == W_K) ? 0 : 1;
       uint16_t* dst = kv + (((size_t)(l * 2 + which) * m.nkv + head) * m.max_seq + pos) * m.hd;
-      stg<uint16_t>(dst + i, f2bf(y0));
-      stg<uint16_t>(dst + i + m.half, f2bf(y1));
+      stc(dst + i, f2bf(y0));
+      stc(dst + i + m.half, f2bf(y1));
     }
   }
 }
@@ -601,7 +622,7 @@ __device__ __forceinline__ void epi_residual(const DevModel& m, const amk_task_t
     if (g.int8) y *= L.stat[r - t.begin];
     const float x = cached ? L.res[r - t.begin] : ldg<float>(m.x + (size_t)xin * m.H + r);
     const float o = x + y;
-    stg<float>(m.x + (size_t)(xin + 1) * m.H + r, o);
+    stc(m.x + (size_t)(xin + 1) * m.H + r, o);
     L.res[r - t.begin] = o;
   }
   if (lane == 0) {
@@ -623,7 +644,7 @@ __device__ __forceinline__ void epi_gateup(const DevModel& m, const amk_task_t& 
       uv *= L.stat[j + 1];
     }
     const float silu = gv / (1.0f + __expf(-gv));
-    stg<float>(m.a + (size_t)t.layer * m.I + r, silu * uv);
+    stc(m.a + (size_t)t.layer * m.I + r, silu * uv);
   }
 }
 
@@ -636,7 +657,7 @@ __device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& 
   for (int r = t.begin + lane; r < t.end; r += 64) {
     float y = row_sum(L.part, m.part_stride, g, wr, r - t.begin) * rs;
     if (g.int8) y *= L.stat[r - t.begin];
-    stg<float>(logits + r, y);
+    stc(logits + r, y);
     if (y > best || (y == best && r < besti)) { best = y; besti = r; }
   }
 #pragma unroll
@@ -645,7 +666,7 @@ __device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& 
     const int oi = __shfl_xor(besti, o);
     if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
   }
-  if (lane == 0) stg<float2>(m.argp + 2 * t.aux, make_float2(best, __int_as_float(besti)));
+  if (lane == 0) stc(reinterpret_cast<float2*>(m.argp + 2 * t.aux), make_float2(best, __int_as_float(besti)));
 }
 
 __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t& t, int lane) {
@@ -662,7 +683,7 @@ __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t
     const int oi = __shfl_xor(besti, o);
     if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
   }
-  if (lane == 0) stg<int32_t>(m.next_token, besti);
+  if (lane == 0) stc(m.next_token, besti);
 }
 
 // ---------------------------------------------------------------- attention (all 8 waves)
@@ -876,10 +897,10 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     }
     if (record) {
       float* rec = dst + h * (kPartHead + HD);
-      stg<float>(rec + kPartHead + d, o);
-      if (d == 0) stg<float2>(rec, make_float2(M, l));
+      stc(rec + kPartHead + d, o);
+      if (d == 0) stc(reinterpret_cast<float2*>(rec), make_float2(M, l));
     } else {
-      stg<float>(dst + h * HD + d, o / l);
+      stc(dst + h * HD + d, o / l);
     }
   }
 }
@@ -952,7 +973,8 @@ __device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g
       const float4 v = red[k * E4 + t];
       o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
     }
-    stg<float4>(m.o + ((size_t)layer * m.nq + (size_t)g * G) * HD + 4 * t, o);
+    float* od = m.o + ((size_t)layer * m.nq + (size_t)g * G) * HD + 4 * t;
+    stc(od, o.x); stc(od + 1, o.y); stc(od + 2, o.z); stc(od + 3, o.w);
   }
 }
 
