@@ -264,12 +264,12 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       free_handle(h);
       return AMK_ERR_UNSUPPORTED;
     }
-    if (amk_internal_prepare(s.hd, s.group, (int)lds_bytes) != AMK_OK) {
+    if (amk_internal_prepare(s.hd, s.group, s.fmt, (int)lds_bytes) != AMK_OK) {
       free_handle(h);
       return AMK_ERR_DEVICE;
     }
     int per_cu = 0;
-    if (amk_internal_occupancy(s.hd, s.group, (int)lds_bytes, &per_cu) != AMK_OK || per_cu < 1) {
+    if (amk_internal_occupancy(s.hd, s.group, s.fmt, (int)lds_bytes, &per_cu) != AMK_OK || per_cu < 1) {
       free_handle(h);
       return AMK_ERR_COOPERATIVE_UNSUPPORTED;
     }

@@ -73,7 +73,7 @@ extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos
 // Threads per workgroup and LDS the kernel needs beyond the model-dependent regions.
 extern "C" int amk_internal_threads(void);
 extern "C" int amk_internal_attn_scratch(int group, int head_dim);
-extern "C" int amk_internal_prepare(int head_dim, int group, int lds_bytes);
-extern "C" int amk_internal_occupancy(int head_dim, int group, int lds_bytes, int* blocks_per_cu);
+extern "C" int amk_internal_prepare(int head_dim, int group, int fmt, int lds_bytes);
+extern "C" int amk_internal_occupancy(int head_dim, int group, int fmt, int lds_bytes, int* blocks_per_cu);
 
 }  // namespace amk

@@ -31,7 +31,7 @@
 // before the result stores, the release or the counter increment would delay
 // every consumer on other CUs; issued after them, the loads stream while the
 // counters propagate and the next input is fetched.  The pipeline is kept
-// shallow (two halves of PIPE granules per wave): measured on the
+// shallow (two halves of Pipe<FMT>::N granules per wave): measured on the
 // Llama-3-8B shape, deeper pipelines both delay the sync wave's polls and
 // input loads and stream no faster.
 //
@@ -56,7 +56,11 @@ namespace amk {
 constexpr int NT = 512;       // threads per workgroup
 constexpr int NW = NT / 64;   // waves
 constexpr int NSW = NW - 1;   // streaming waves
-constexpr int PIPE = 4;       // 1-KiB granules per pipeline half, per wave
+// Granules per pipeline half, per wave: 4 for bf16 weights, 2 for int8 (an
+// int8 granule holds twice the multiply-adds).  Measured on the Llama-3-8B
+// shape, deeper pipelines delay the sync wave's polls and input loads and
+// stream no faster.
+template <int FMT> struct Pipe { static constexpr int N = FMT == AMK_WEIGHTS_W8A16 ? 2 : 4; };
 constexpr int GRAN = 1024;    // bytes per wave-wide 16-B-per-lane load
 
 struct Ctl {
@@ -297,11 +301,12 @@ __device__ __forceinline__ uint4 load_gran(const Cursor& cu, const Gemv& g, int 
   return ldg<uint4>(cu.p + off);
 }
 
-// Issue PIPE granules starting at global granule index gi (clipped to g1).
-__device__ __forceinline__ void issue_block(uint4 (&buf)[PIPE], Cursor& cu, int& gi, int g1, const DevModel& m,
+// Issue N granules starting at global granule index gi (clipped to g1).
+template <int N>
+__device__ __forceinline__ void issue_block(uint4 (&buf)[N], Cursor& cu, int& gi, int g1, const DevModel& m,
                                             const amk_task_t& t, const Gemv& g, int lane) {
 #pragma unroll
-  for (int i = 0; i < PIPE; ++i) {
+  for (int i = 0; i < N; ++i) {
     buf[i] = load_gran(cu, g, lane);
     if (gi < g1) cursor_next(cu, m, t, g);
     ++gi;
@@ -336,12 +341,13 @@ __device__ __forceinline__ float dot_gran(const uint4 v, const float* __restrict
   return acc;
 }
 
-// Consume PIPE granules; a finished row's wave-reduced partial goes to part[j].
-__device__ __forceinline__ void consume_block(const uint4 (&buf)[PIPE], int& j, int& c, int& gi, int g1, float& acc,
+// Consume N granules; a finished row's wave-reduced partial goes to part[j].
+template <int N>
+__device__ __forceinline__ void consume_block(const uint4 (&buf)[N], int& j, int& c, int& gi, int g1, float& acc,
                                               const float* __restrict__ act, float* __restrict__ part,
                                               const Gemv& g, int lane) {
 #pragma unroll
-  for (int i = 0; i < PIPE; ++i) {
+  for (int i = 0; i < N; ++i) {
     if (gi < g1) {
       uint4 v = buf[i];
       if (g.tail && c * GRAN + lane * 16 >= g.row_bytes) v = make_uint4(0, 0, 0, 0);
@@ -979,10 +985,11 @@ __device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g
 }
 
 // ---------------------------------------------------------------- the kernel
-template <int HD, int GM>
+template <int HD, int GM, int FMT>
 __global__ void __launch_bounds__(NT, 1)
 amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16_t* __restrict__ kv,
                   float* __restrict__ logits, uint64_t timeout_ticks) {
+  constexpr int PIPE = Pipe<FMT>::N;
   extern __shared__ float4 lds4[];
   __shared__ Ctl ctl;
   Lds L;
@@ -1152,14 +1159,15 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
 
 // ---------------------------------------------------------------- host side
 template <int HD, int GM>
-static const void* kernel_ptr() {
-  return (const void*)amk_decode_kernel<HD, GM>;
+static const void* kernel_ptr(int fmt) {
+  return fmt == AMK_WEIGHTS_W8A16 ? (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W8A16>
+                                  : (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_BF16>;
 }
 
-static const void* kernel_for(int head_dim, int group) {
+static const void* kernel_for(int head_dim, int group, int fmt) {
   const bool small = group <= 4;
-  if (head_dim == 64) return small ? kernel_ptr<64, 4>() : kernel_ptr<64, 8>();
-  return small ? kernel_ptr<128, 4>() : kernel_ptr<128, 8>();
+  if (head_dim == 64) return small ? kernel_ptr<64, 4>(fmt) : kernel_ptr<64, 8>(fmt);
+  return small ? kernel_ptr<128, 4>(fmt) : kernel_ptr<128, 8>(fmt);
 }
 
 extern "C" int amk_internal_threads(void) { return NT; }
@@ -1172,16 +1180,16 @@ extern "C" int amk_internal_attn_scratch(int group, int head_dim) {
   return small ? AttnGeom<128, 4>::LDS : AttnGeom<128, 8>::LDS;
 }
 
-extern "C" int amk_internal_prepare(int head_dim, int group, int lds_bytes) {
+extern "C" int amk_internal_prepare(int head_dim, int group, int fmt, int lds_bytes) {
   hipError_t e =
-      hipFuncSetAttribute(kernel_for(head_dim, group), hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+      hipFuncSetAttribute(kernel_for(head_dim, group, fmt), hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }
 
 // Largest number of co-resident workgroups of the kernel per CU for this LDS size.
-extern "C" int amk_internal_occupancy(int head_dim, int group, int lds_bytes, int* blocks_per_cu) {
+extern "C" int amk_internal_occupancy(int head_dim, int group, int fmt, int lds_bytes, int* blocks_per_cu) {
   hipError_t e =
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, kernel_for(head_dim, group), NT, lds_bytes);
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, kernel_for(head_dim, group, fmt), NT, lds_bytes);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }
 
@@ -1189,7 +1197,7 @@ extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos
                                    float* logits, uint64_t timeout_ticks, void* stream) {
   DevModel mm = *m;
   void* args[] = {&mm, &token, &pos, &epoch, &kv, &logits, &timeout_ticks};
-  hipError_t e = hipLaunchCooperativeKernel(kernel_for(m->hd, m->group), dim3(m->n_cu), dim3(NT), args,
+  hipError_t e = hipLaunchCooperativeKernel(kernel_for(m->hd, m->group, m->fmt), dim3(m->n_cu), dim3(NT), args,
                                             (unsigned)m->lds_bytes, (hipStream_t)stream);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }
