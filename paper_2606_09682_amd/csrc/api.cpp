@@ -246,14 +246,14 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       return AMK_ERR_SCHEDULE_REJECTED;
     }
 
-    // LDS: activation vector (padded to a whole int8 granule), norm gain,
-    // static per-row data, residual rows, partials / attention scratch
+    // LDS: activation vector (padded to a whole int8 granule), static
+    // per-row data, residual rows, partials / attention scratch
     const int nsw = amk_internal_threads() / 64 - 1;
     const size_t act = round_up((size_t)std::max({s.H, s.nq * s.hd, s.I}), 1024);
     // per-wave partial stride in whole float4s keeps every region 16-byte aligned
     const size_t pstride = round_up((size_t)s.max_jobs, 4);
     const size_t scr = std::max<size_t>((size_t)nsw * pstride, (size_t)amk_internal_attn_scratch(s.group, s.hd));
-    const size_t lds_bytes = (act + s.H + 3 * pstride + scr) * 4;
+    const size_t lds_bytes = (act + 3 * pstride + scr) * 4;
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
       free_handle(h);

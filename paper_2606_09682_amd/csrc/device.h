@@ -59,7 +59,7 @@ struct DevModel {
   uint64_t* trace;           // [n_tasks][AMK_TRACE_FIELDS] timestamps, or null
   const amk_task_t* tasks;   // sorted by (cu, seq)
   const int32_t* queue_start;// [n_cu + 1]
-  // LDS layout (floats): act[lds_act] gain[H] stat[2 * part_stride]
+  // LDS layout (floats): act[lds_act] stat[2 * part_stride]
   // res[part_stride] part[lds_scr]
   int32_t lds_act;           // activation vector region (padded to 1024, zero-filled tail)
   int32_t part_stride;       // rows of one GEMV task at most (partials per streaming wave)

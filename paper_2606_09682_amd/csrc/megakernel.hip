@@ -427,12 +427,11 @@ __device__ __forceinline__ bool release_signal_last(const DevModel& m, int count
   return (int32_t)(old + 1u - target) == 0;
 }
 
-// ---------------------------------------------------------------- static per-task data
-// Data that does not depend on this launch's results (norm gains, RoPE
-// factors, int8 row scales, the layer-0 embedding rows) is fetched before
-// the task's counter wait, so the critical path after the wait only moves the
-// input activation.  LDS regions after the activation:
-//   gain[H]                 RMSNorm gain of a normed input, fp32
+// ---------------------------------------------------------------- per-row static data
+// Data of a GEMV task that does not depend on this launch's results and is
+// needed only in its epilogue (int8 row scales, RoPE factors, the layer-0
+// embedding rows of the residual) is fetched by the sync wave while the
+// streaming waves compute.  LDS regions after the activation:
 //   stat[2 * max_rows]      int8 row scales (rows [0, nj)), then for QKV the
 //                           RoPE (cos, sin) of unit u at [nj + 2u, nj + 2u + 1]
 //   res[max_rows]           residual rows of the last O / down task (or the
@@ -440,26 +439,14 @@ __device__ __forceinline__ bool release_signal_last(const DevModel& m, int count
 //   part[...]               per-streaming-wave row partials / attention scratch
 struct Lds {
   float* act;
-  float* gain;
   float* stat;
   float* res;
   float* part;
 };
 
-__device__ __forceinline__ void load_static(const DevModel& m, const amk_task_t& t, int token, int pos,
-                                            const Lds& L, Ctl& ctl, int lane) {
+__device__ __forceinline__ void load_rowdata(const DevModel& m, const amk_task_t& t, int token, int pos,
+                                             const Lds& L, Ctl& ctl, int lane) {
   const int op = t.op;
-  if (is_normed(op)) {
-    const uint16_t* g = op == AMK_OP_QKV ? ldc<const uint16_t*>(&m.layers[t.layer].attn_norm)
-                        : op == AMK_OP_GATEUP ? ldc<const uint16_t*>(&m.layers[t.layer].mlp_norm)
-                                              : m.final_norm;
-    for (int e = lane * 8; e < m.H; e += 512) {
-      const uint4 w = ldg<uint4>(g + e);
-      *reinterpret_cast<float4*>(L.gain + e) = make_float4(bf_lo(w.x), bf_hi(w.x), bf_lo(w.y), bf_hi(w.y));
-      *reinterpret_cast<float4*>(L.gain + e + 4) = make_float4(bf_lo(w.z), bf_hi(w.z), bf_lo(w.w), bf_hi(w.w));
-    }
-  }
-  if (!is_gemv(op)) return;
   const Gemv g = gemv_geom(m, t);
   if (g.int8) {
     for (int j = lane; j < g.nj; j += 64) {
@@ -490,21 +477,26 @@ __device__ __forceinline__ void load_static(const DevModel& m, const amk_task_t&
 
 // ---------------------------------------------------------------- input activation (all waves)
 // The task input moves into LDS in one round trip: wave w copies a 1/8 slice.
-// Normed inputs store x * gain and leave each wave's sum of x^2 in ctl.ssq;
-// the GEMV result is scaled by 1/sqrt(mean(x^2) + eps) in the epilogue
-// (RMSNorm folded into the consumer).
+// Normed inputs load the RMSNorm gain in the same round trip, store x * gain
+// and leave each wave's sum of x^2 in ctl.ssq; the GEMV result is scaled by
+// 1/sqrt(mean(x^2) + eps) in the epilogue (RMSNorm folded into the consumer).
 __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& t, int token, const Lds& L, Ctl& ctl,
                                            int wave, int lane) {
   const int op = t.op;
   const float* src = nullptr;
   const uint16_t* src_bf = nullptr;
+  const uint16_t* gain = nullptr;
   switch (op) {
     case AMK_OP_QKV:
       if (t.layer == 0) src_bf = m.embed + (size_t)token * m.H;
       else src = m.x + (size_t)(2 * t.layer) * m.H;
+      gain = ldc<const uint16_t*>(&m.layers[t.layer].attn_norm);
       break;
-    case AMK_OP_GATEUP: src = m.x + (size_t)(2 * t.layer + 1) * m.H; break;
-    case AMK_OP_LMHEAD: src = m.x + (size_t)(2 * m.L) * m.H; break;
+    case AMK_OP_GATEUP:
+      src = m.x + (size_t)(2 * t.layer + 1) * m.H;
+      gain = ldc<const uint16_t*>(&m.layers[t.layer].mlp_norm);
+      break;
+    case AMK_OP_LMHEAD: src = m.x + (size_t)(2 * m.L) * m.H; gain = m.final_norm; break;
     case AMK_OP_O: src = m.o + (size_t)t.layer * m.nq * m.hd; break;
     case AMK_OP_DOWN: src = m.a + (size_t)t.layer * m.I; break;
     default: return;
@@ -512,11 +504,11 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
   const int K = task_k(m, t);
   const int n4 = K >> 2;  // float4 vectors (K is a multiple of 16)
   const int v0 = (n4 * wave) / NW, v1 = (n4 * (wave + 1)) / NW;
-  const bool normed = is_normed(op);
   float ss = 0.f;
   constexpr int NB = 8;
   for (int b = v0; b < v1; b += NB * 64) {
     float4 xv[NB];
+    uint2 gv[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int v = b + i * 64 + lane;
@@ -527,6 +519,7 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
         } else {
           xv[i] = ldg<float4>(src + (size_t)v * 4);
         }
+        if (gain) gv[i] = ldg<uint2>(gain + (size_t)v * 4);
       }
     }
 #pragma unroll
@@ -534,16 +527,15 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
       const int v = b + i * 64 + lane;
       if (v < v1) {
         float4 x = xv[i];
-        if (normed) {
+        if (gain) {
           ss = fmaf(x.x, x.x, ss); ss = fmaf(x.y, x.y, ss); ss = fmaf(x.z, x.z, ss); ss = fmaf(x.w, x.w, ss);
-          const float4 g = *reinterpret_cast<const float4*>(L.gain + v * 4);
-          x = make_float4(x.x * g.x, x.y * g.y, x.z * g.z, x.w * g.w);
+          x = make_float4(x.x * bf_lo(gv[i].x), x.y * bf_hi(gv[i].x), x.z * bf_lo(gv[i].y), x.w * bf_hi(gv[i].y));
         }
         *reinterpret_cast<float4*>(L.act + v * 4) = x;
       }
     }
   }
-  if (normed) {
+  if (gain) {
     ss = wave_sum(ss);
     if (lane == 0) ctl.ssq[wave] = ss;
   }
@@ -994,8 +986,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
   __shared__ Ctl ctl;
   Lds L;
   L.act = reinterpret_cast<float*>(lds4);
-  L.gain = L.act + m.lds_act;
-  L.stat = L.gain + m.H;
+  L.stat = L.act + m.lds_act;
   L.res = L.stat + 2 * m.part_stride;
   L.part = L.res + m.part_stride;
 
@@ -1039,10 +1030,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     }
   };
 
-  if (qb < qe) {
-    if (wave == 0) load_static(m, ldc<amk_task_t>(m.tasks + qb), token, pos, L, ctl, lane);
-    else prefetch(qb);
-  }
+  if (qb < qe && wave != 0) prefetch(qb);
   __syncthreads();
 
   for (int idx = qb; idx < qe; ++idx) {
@@ -1075,7 +1063,8 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     }
     if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());
 
-    // ---- compute
+    // ---- compute (the sync wave meanwhile fetches the epilogue's row data)
+    if (gemv && wave == 0) load_rowdata(m, t, token, pos, L, ctl, lane);
     if (gemv && wave != 0 && g0 < g1) {
       const int sw = wave - 1;
       float* mypart = L.part + sw * pstride;
@@ -1148,12 +1137,8 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
       stg<uint64_t>(tr + AMK_TRACE_CHAINED, 0ull);
     }
 
-    // ---- the next task's static data (sync wave) and weight stream (streaming waves)
-    if (wave == 0) {
-      if (idx + 1 < qe) load_static(m, ldc<amk_task_t>(m.tasks + idx + 1), token, pos, L, ctl, lane);
-    } else {
-      prefetch(idx + 1);
-    }
+    // ---- the next task's weight stream (streaming waves)
+    if (wave != 0) prefetch(idx + 1);
   }
 }
 
