@@ -144,6 +144,27 @@ __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, false));
 }
 
+// Exchanges with lane ^ 16 and lane ^ 32 through the gfx950 row swaps: with
+// both operands v, v_permlane16_swap returns (v[l], v[l ^ 16]) in even rows
+// of 16 lanes and (v[l ^ 16], v[l]) in odd rows (v_permlane32_swap likewise
+// for halves of 32), so one swap and one VALU op combine the two lanes.
+__device__ __forceinline__ float xor16_add(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor16_max(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_add(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Sum over groups of N consecutive lanes (N in 2, 4, 8, 16, 32); every lane of
 // a group receives its group's sum.
 template <int N>
@@ -153,7 +174,7 @@ __device__ __forceinline__ float group_sum(float v) {
   if constexpr (N >= 4) v += dpp<0x4e>(v);
   if constexpr (N >= 8) v += dpp<0x141>(v);
   if constexpr (N >= 16) v += dpp<0x140>(v);
-  if constexpr (N >= 32) v += __shfl_xor(v, 16);
+  if constexpr (N >= 32) v = xor16_add(v);
   return v;
 }
 template <int N>
@@ -162,7 +183,26 @@ __device__ __forceinline__ float group_max(float v) {
   if constexpr (N >= 4) v = fmaxf(v, dpp<0x4e>(v));
   if constexpr (N >= 8) v = fmaxf(v, dpp<0x141>(v));
   if constexpr (N >= 16) v = fmaxf(v, dpp<0x140>(v));
-  if constexpr (N >= 32) v = fmaxf(v, __shfl_xor(v, 16));
+  if constexpr (N >= 32) v = xor16_max(v);
+  return v;
+}
+
+// Sum / max over the lanes l ^ k*G of a wave (G = 8, 16 or 32: the lanes that
+// share l mod G), returned to every lane.
+template <int G>
+__device__ __forceinline__ float across_sum(float v) {
+  static_assert(G == 8 || G == 16 || G == 32 || G == 64, "group stride");
+  if constexpr (G == 8) v += dpp<0x128>(v);  // row_ror:8 = lane ^ 8 within a row of 16
+  if constexpr (G <= 16) v = xor16_add(v);
+  if constexpr (G <= 32) v = xor32_add(v);
+  return v;
+}
+template <int G>
+__device__ __forceinline__ float across_max(float v) {
+  static_assert(G == 8 || G == 16 || G == 32 || G == 64, "group stride");
+  if constexpr (G == 8) v = fmaxf(v, dpp<0x128>(v));
+  if constexpr (G <= 16) v = xor16_max(v);
+  if constexpr (G <= 32) v = xor32_max(v);
   return v;
 }
 
@@ -175,8 +215,8 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 __device__ __forceinline__ float wave_max(float v) {
   v = group_max<16>(v);
-  v = fmaxf(v, __shfl_xor(v, 16));
-  v = fmaxf(v, __shfl_xor(v, 32));
+  v = xor16_max(v);
+  v = xor32_max(v);
   return v;
 }
 
@@ -857,18 +897,12 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
   for (int h = 0; h < GM; ++h) {
     if (h < G) {
       // merge the row groups of the wave: rescale each to the wave's max
-      float M = m_run[h];
-#pragma unroll
-      for (int o = LPR; o < 64; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
+      const float M = across_max<LPR>(m_run[h]);
       const float f = m_run[h] == -INFINITY ? 0.f : __expf(m_run[h] - M);
-      float l = l_run[h] * f;
-#pragma unroll
-      for (int o = LPR; o < 64; o <<= 1) l += __shfl_xor(l, o);
+      const float l = across_sum<LPR>(l_run[h] * f);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
-        float v = acc[h][e] * f;
-#pragma unroll
-        for (int o = LPR; o < 64; o <<= 1) v += __shfl_xor(v, o);
+        const float v = across_sum<LPR>(acc[h][e] * f);
         if (sub == 0) red[(wave * GM + h) * HD + c * EPL + e] = v;
       }
       if (lane == 0) {
