@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define AMK_ABI_VERSION 2
+#define AMK_ABI_VERSION 3
 
 /* ---- status codes ------------------------------------------------------ */
 enum {
@@ -105,12 +105,19 @@ typedef struct {
 /* Optional tuning; zero fields take defaults. */
 typedef struct {
   int32_t attn_splits;      /* attention tasks per KV head (1..64); 0 = derived from the CU count */
-  int32_t timeout_us;       /* deadline of one device counter wait in microseconds; 0 = 2 s */
+  int32_t timeout_us;       /* deadline of one decode step in microseconds, on each workgroup's
+                               clock from its start: a counter wait still unsatisfied past it
+                               stops the launch with AMK_ERR_TIMEOUT; 0 = 2 s */
   int32_t max_rows_per_task;/* cap on rows of one GEMV task; 0 = 1024 */
   int32_t trace;            /* 1: record per-task timestamps (see amk_trace_copy) */
   int32_t short_context;    /* steps with pos + 1 <= short_context run the short-context schedule
                                (AMK_SCHEDULE_SHORT); 0 = 256; negative = never */
+  int32_t tiny_context;     /* steps with pos + 1 <= tiny_context (at most AMK_TINY_MAX) run the
+                               tiny-context schedule (AMK_SCHEDULE_TINY); 0 = 6; negative = never */
 } amk_tuning_t;
+
+/* Largest tiny_context: the tiny schedule's attention keeps every position in registers. */
+#define AMK_TINY_MAX 8
 
 typedef struct amk_handle_s* amk_handle_t;
 
@@ -199,13 +206,15 @@ int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_t
 
 /* ---- schedule introspection (CPU only, no device needed) -------------------- */
 
-/* Schedule variants.  Both compute the same step; they differ in where the
+/* Schedule variants.  All compute the same step; they differ in where the
  * attention runs.  SHORT: the last QKV task of each KV group to finish runs
  * that group's whole attention inline (no attention stage).  LONG: the
  * attention of each KV group is split over `attn_splits` position ranges on
  * as many queues (flash-decoding style), and the last split of a group to
- * finish merges the splits inline. */
-enum { AMK_SCHEDULE_SHORT = 0, AMK_SCHEDULE_LONG = 1 };
+ * finish merges the splits inline.  TINY (at most AMK_TINY_MAX positions):
+ * every O task computes the attention of all query heads itself, straight
+ * from q and the KV cache, and waits only for the QKV stage. */
+enum { AMK_SCHEDULE_SHORT = 0, AMK_SCHEDULE_LONG = 1, AMK_SCHEDULE_TINY = 2 };
 
 /* Operations of the task graph, in the order of one layer.
  * QKV units: unit u is the RoPE row pair (i, i + d/2), i = u % (d/2), of head
@@ -217,7 +226,8 @@ enum {
   AMK_OP_ATTN = 2,     /* attention of KV group `aux` over position split `begin` of `end` splits; queued
                           splits leave partial results, the inline task (begin 0, end 1) the output */
   AMK_OP_COMBINE = 3,  /* merge the position splits of query heads [begin, end) (inline, see below) */
-  AMK_OP_O = 4,        /* rows [begin, end) of x1 = x + Wo o */
+  AMK_OP_O = 4,        /* rows [begin, end) of x1 = x + Wo o; aux 1: o is first computed by the task
+                          itself from q and the KV cache (tiny schedule) */
   AMK_OP_GATEUP = 5,   /* rows [begin, end) of a = silu(Wg h2) * (Wu h2), h2 = RMSNorm(x1) */
   AMK_OP_DOWN = 6,     /* rows [begin, end) of x2 = x1 + Wd a */
   AMK_OP_LMHEAD = 7,   /* rows [begin, end) of logits = W_lm RMSNorm(x); argmax partial slot `aux` */

@@ -24,6 +24,9 @@ using amk::amk_internal_occupancy;
 using amk::amk_internal_prepare;
 using amk::amk_internal_threads;
 
+constexpr int kVariants = 3;
+bool valid_variant(int v) { return v >= 0 && v < kVariants; }
+
 // One schedule variant as uploaded: device task table, queue offsets, trace.
 // Each variant owns its counters and epoch: a counter's target is
 // epoch * (its producers per launch), which holds only while every launch
@@ -40,8 +43,8 @@ struct DevSchedule {
 struct amk_handle_s {
   Shape s;
   int device = 0;
-  Schedule sch[2];              // AMK_SCHEDULE_SHORT, AMK_SCHEDULE_LONG
-  DevSchedule dsch[2];
+  Schedule sch[kVariants];      // AMK_SCHEDULE_SHORT, _LONG, _TINY
+  DevSchedule dsch[kVariants];
   int last_variant = -1;
   DevModel dm;
   void* d_block = nullptr;      // one device allocation for tables and scratch
@@ -115,7 +118,7 @@ size_t amk_kv_cache_bytes(const amk_config_t* cfg) {
 
 int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
                       int32_t* n_tasks, int32_t* n_counters) {
-  if (variant != AMK_SCHEDULE_SHORT && variant != AMK_SCHEDULE_LONG) return AMK_ERR_INVALID_ARGUMENT;
+  if (!valid_variant(variant)) return AMK_ERR_INVALID_ARGUMENT;
   try {
     Shape s;
     int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
@@ -133,7 +136,7 @@ int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32
 
 int amk_schedule_export(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
                         amk_task_t* tasks, int32_t cap, int32_t* n_tasks, int32_t* n_counters) {
-  if (variant != AMK_SCHEDULE_SHORT && variant != AMK_SCHEDULE_LONG) return AMK_ERR_INVALID_ARGUMENT;
+  if (!valid_variant(variant)) return AMK_ERR_INVALID_ARGUMENT;
   try {
     Shape s;
     int st = amk::derive_shape(cfg, tuning, n_cu, &s, nullptr);
@@ -172,7 +175,7 @@ int amk_check_config(const amk_config_t* cfg, int32_t n_cu) {
     Shape s;
     int st = amk::derive_shape(cfg, nullptr, n_cu, &s, nullptr);
     if (st != AMK_OK) return st;
-    for (int v = AMK_SCHEDULE_SHORT; v <= AMK_SCHEDULE_LONG; ++v) {
+    for (int v = 0; v < kVariants; ++v) {
       Schedule sch = amk::build_schedule(s, n_cu, v);
       amk_check_report_t rep;
       if (!amk::check_schedule(s, n_cu, sch.tasks.data(), (int)sch.tasks.size(), sch.n_counters, &rep))
@@ -230,7 +233,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     h = new amk_handle_s();
     h->s = s;
     h->device = dev;
-    for (int v = AMK_SCHEDULE_SHORT; v <= AMK_SCHEDULE_LONG; ++v) {
+    for (int v = 0; v < kVariants; ++v) {
       h->sch[v] = amk::build_schedule(s, n_cu, v);
       amk_check_report_t rep;
       if (!amk::check_schedule(s, n_cu, h->sch[v].tasks.data(), (int)h->sch[v].tasks.size(), h->sch[v].n_counters,
@@ -241,7 +244,8 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       }
     }
     const Schedule& sl = h->sch[AMK_SCHEDULE_LONG];
-    if (sl.n_lm_slots != h->sch[AMK_SCHEDULE_SHORT].n_lm_slots) {  // the argmax slots are shared
+    if (sl.n_lm_slots != h->sch[AMK_SCHEDULE_SHORT].n_lm_slots ||
+        sl.n_lm_slots != h->sch[AMK_SCHEDULE_TINY].n_lm_slots) {  // the argmax slots are shared
       free_handle(h);
       return AMK_ERR_SCHEDULE_REJECTED;
     }
@@ -292,8 +296,8 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     const Region r_next = take(sizeof(int32_t));
     const Region r_abort = take(sizeof(int32_t));
     const bool tracing = tuning && tuning->trace;
-    Region r_tasks[2], r_queue[2], r_trace[2], r_ctr[2];
-    for (int v = 0; v < 2; ++v) {
+    Region r_tasks[kVariants], r_queue[kVariants], r_trace[kVariants], r_ctr[kVariants];
+    for (int v = 0; v < kVariants; ++v) {
       r_ctr[v] = take(sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch[v].n_counters);
       r_tasks[v] = take(sizeof(amk_task_t) * h->sch[v].tasks.size());
       r_queue[v] = take(sizeof(int32_t) * h->sch[v].queue_start.size());
@@ -350,7 +354,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     }
     bool ok = hipMemcpy(base + r_layers.off, layers.data(), r_layers.bytes, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(base + r_rope.off, rope.data(), r_rope.bytes, hipMemcpyHostToDevice) == hipSuccess;
-    for (int v = 0; v < 2 && ok; ++v)
+    for (int v = 0; v < kVariants && ok; ++v)
       ok = hipMemcpy(base + r_tasks[v].off, h->sch[v].tasks.data(), r_tasks[v].bytes, hipMemcpyHostToDevice) ==
                hipSuccess &&
            hipMemcpy(base + r_queue[v].off, h->sch[v].queue_start.data(), r_queue[v].bytes, hipMemcpyHostToDevice) ==
@@ -391,7 +395,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.dev_abort = (int32_t*)(base + r_abort.off);
     m.host_status = d_status;
     m.host_abort = d_hab;
-    for (int v = 0; v < 2; ++v) {
+    for (int v = 0; v < kVariants; ++v) {
       h->dsch[v].tasks = (const amk_task_t*)(base + r_tasks[v].off);
       h->dsch[v].queue_start = (const int32_t*)(base + r_queue[v].off);
       h->dsch[v].trace = tracing ? (uint64_t*)(base + r_trace[v].off) : nullptr;
@@ -424,7 +428,9 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   if (sticky != 0) return sticky;
   DeviceGuard guard(h->device);
   if (!guard.ok) return AMK_ERR_DEVICE;
-  const int variant = pos + 1 <= h->s.short_context ? AMK_SCHEDULE_SHORT : AMK_SCHEDULE_LONG;
+  const int variant = pos + 1 <= h->s.tiny_context    ? AMK_SCHEDULE_TINY
+                      : pos + 1 <= h->s.short_context ? AMK_SCHEDULE_SHORT
+                                                      : AMK_SCHEDULE_LONG;
   DevSchedule& ds = h->dsch[variant];
   DevModel m = h->dm;
   m.tasks = ds.tasks;

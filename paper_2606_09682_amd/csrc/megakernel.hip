@@ -406,7 +406,7 @@ __device__ __forceinline__ void consume_block(const uint4 (&buf)[N], int& j, int
 
 // ---------------------------------------------------------------- sync wave: counters
 __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t, const amk_task_t* tp, uint32_t epoch,
-                                          uint64_t timeout_ticks, int lane, uint64_t* tr) {
+                                          uint64_t deadline, int lane, uint64_t* tr) {
   const int nw = t.n_wait;
   if (nw == 0) return __hip_atomic_load(m.dev_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
   uint32_t* p = nullptr;
@@ -415,30 +415,28 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
     p = m.counters + (size_t)ldg<int32_t>(&tp->wait_counter[lane]) * kCounterStride;
     target = epoch * (uint32_t)ldg<int32_t>(&tp->wait_count[lane]);
   }
-  const uint64_t t0 = wall_clock64();
   uint32_t spins = 0;
   for (;;) {
     bool ok = true;
     if (lane < nw) ok = (int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) >= 0;
+    const uint64_t now = wall_clock64();
     if (__all(ok)) break;
     if (__hip_atomic_load(m.dev_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
-    ++spins;
-    if ((spins & 7u) == 0) {
-      // host-mapped flag: read over the bus, so only every 64 spins
-      int code = 0;
-      if ((spins & 63u) == 0 && __hip_atomic_load(m.host_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM))
-        code = AMK_ERR_ABORTED;
-      else if (wall_clock64() - t0 > timeout_ticks)
-        code = AMK_ERR_TIMEOUT;
-      if (code) {
-        if (lane == 0) {
-          // plain stores (no read-modify-write over the bus); if two
-          // workgroups stop at once, either code is a valid report
-          __hip_atomic_store(m.host_status, code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-          __hip_atomic_store(m.dev_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        return false;
+    int code = 0;
+    // host-mapped flag: read over the bus, so only every 64 spins
+    if ((++spins & 63u) == 0 &&
+        __hip_atomic_load(m.host_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM))
+      code = AMK_ERR_ABORTED;
+    else if (now > deadline)
+      code = AMK_ERR_TIMEOUT;
+    if (code) {
+      if (lane == 0) {
+        // plain stores (no read-modify-write over the bus); if two
+        // workgroups stop at once, either code is a valid report
+        __hip_atomic_store(m.host_status, code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(m.dev_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      return false;
     }
     __builtin_amdgcn_s_sleep(1);
   }
@@ -937,6 +935,78 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
   }
 }
 
+// Attention of every query head over positions [0, pos] (pos < AMK_TINY_MAX)
+// into act[h * HD + d]: the input of an O task of the tiny schedule, which
+// computes it itself instead of waiting for an attention stage.  Each wave
+// takes HR heads per round; lane owns head dims [lane * DPL, (lane + 1) * DPL).
+// All q / K / V loads of a round go out before any arithmetic; positions past
+// pos re-read row pos (clamped, unused).
+template <int HD>
+__device__ __forceinline__ void attention_all(const DevModel& m, int layer, int pos, const uint16_t* __restrict__ kv,
+                                              float* __restrict__ act, int wave, int lane) {
+  constexpr int DPL = HD / 64;
+  constexpr int HR = 4;
+  constexpr int T = AMK_TINY_MAX;
+  const int n = pos + 1;
+  const size_t hs = (size_t)m.max_seq * HD;
+  for (int h0 = wave * HR; h0 < m.nq; h0 += NW * HR) {
+    float qv[HR][DPL];
+    uint32_t kr[HR][T], vr[HR][T];  // DPL bf16 values per row (the low half only when DPL == 1)
+#pragma unroll
+    for (int i = 0; i < HR; ++i) {
+      const int h = min(h0 + i, m.nq - 1);
+      const int g = h / m.group;
+      const float* qh = m.q + ((size_t)layer * m.nq + h) * HD + lane * DPL;
+      const uint16_t* Kp = kv + ((size_t)(layer * 2) * m.nkv + g) * hs + lane * DPL;
+      const uint16_t* Vp = kv + ((size_t)(layer * 2 + 1) * m.nkv + g) * hs + lane * DPL;
+      if constexpr (DPL == 2) {
+        const float2 q2 = ldg<float2>(qh);
+        qv[i][0] = q2.x;
+        qv[i][1] = q2.y;
+      } else {
+        qv[i][0] = ldg<float>(qh);
+      }
+#pragma unroll
+      for (int p = 0; p < T; ++p) {
+        const size_t off = (size_t)min(p, n - 1) * HD;
+        if constexpr (DPL == 2) {
+          kr[i][p] = ldg<uint32_t>(Kp + off);
+          vr[i][p] = ldg<uint32_t>(Vp + off);
+        } else {
+          kr[i][p] = ldg<uint16_t>(Kp + off);
+          vr[i][p] = ldg<uint16_t>(Vp + off);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < HR; ++i) {
+      float mrun = -INFINITY, l = 0.f, acc[DPL];
+#pragma unroll
+      for (int j = 0; j < DPL; ++j) acc[j] = 0.f;
+#pragma unroll
+      for (int p = 0; p < T; ++p) {
+        if (p < n) {
+          float d = qv[i][0] * bf_lo(kr[i][p]);
+          if constexpr (DPL == 2) d = fmaf(qv[i][1], bf_hi(kr[i][p]), d);
+          d = wave_sum(d) * m.attn_scale;
+          const float mn = fmaxf(mrun, d);
+          const float alpha = __expf(mrun - mn), e = __expf(d - mn);
+          l = l * alpha + e;
+          acc[0] = fmaf(e, bf_lo(vr[i][p]), acc[0] * alpha);
+          if constexpr (DPL == 2) acc[1] = fmaf(e, bf_hi(vr[i][p]), acc[1] * alpha);
+          mrun = mn;
+        }
+      }
+      const int h = h0 + i;
+      if (h < m.nq) {
+        const float inv = 1.0f / l;
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) act[h * HD + lane * DPL + j] = acc[j] * inv;
+      }
+    }
+  }
+}
+
 // Number of position splits with work at `pos` (split s covers positions
 // [s * chunk, (s + 1) * chunk) of 0..pos).
 __device__ __forceinline__ int active_splits(const DevModel& m, int pos, int* chunk_out) {
@@ -1064,6 +1134,8 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     }
   };
 
+  // the step's deadline, on this workgroup's clock from its start
+  const uint64_t deadline = wall_clock64() + timeout_ticks;
   if (qb < qe && wave != 0) prefetch(qb);
   __syncthreads();
 
@@ -1077,7 +1149,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     // ---- B1a: the sync wave's counter wait
     if (wave == 0) {
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_WAIT_BEGIN, (uint64_t)wall_clock64());
-      const bool ok = wait_deps(m, t, m.tasks + idx, epoch, timeout_ticks, lane, tr);
+      const bool ok = wait_deps(m, t, m.tasks + idx, epoch, deadline, lane, tr);
       if (!ok && lane == 0) ctl.abort = 1;
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_WAIT_END, (uint64_t)wall_clock64());
     }
@@ -1092,7 +1164,8 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
 
     // ---- B1b: every wave moves its slice of the input activation
     if (gemv) {
-      load_input(m, t, token, L, ctl, wave, lane);
+      if (t.op == AMK_OP_O && t.aux == 1) attention_all<HD>(m, t.layer, pos, kv, L.act, wave, lane);
+      else load_input(m, t, token, L, ctl, wave, lane);
       __syncthreads();
     }
     if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());

@@ -87,6 +87,12 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
   }
   const int sc = tuning ? tuning->short_context : 0;
   s->short_context = sc == 0 ? kDefaultShortContext : sc < 0 ? 0 : sc;
+  const int tc = tuning ? tuning->tiny_context : 0;
+  if (tc > AMK_TINY_MAX) {
+    set_msg(why, "tiny_context %ld above %ld", tc, AMK_TINY_MAX);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  s->tiny_context = tc == 0 ? kDefaultTinyContext : tc < 0 ? 0 : tc;
   return AMK_OK;
 }
 
@@ -162,24 +168,37 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
     return std::make_pair(sig, n);
   };
 
-  const bool shortv = variant == AMK_SCHEDULE_SHORT;
+  const bool shortv = variant == AMK_SCHEDULE_SHORT, tinyv = variant == AMK_SCHEDULE_TINY;
   int prev_c = -1, prev_n = 0;  // counter of the stage producing the layer input
   for (int l = 0; l < s.L; ++l) {
     // QKV: npg tasks per KV group over that group's units; each group's tasks
-    // signal the group's counter.
+    // signal the group's counter (tiny schedule: one counter for the stage).
     const int c_qkv0 = n_ctr;
-    n_ctr += s.nkv;
-    const int c_done = n_ctr++;  // every KV group's attention output is written
+    n_ctr += tinyv ? 1 : s.nkv;
+    const int c_done = tinyv ? -1 : n_ctr++;  // every KV group's attention output is written
     const int n_qkv = s.nkv * s.npg;
     for (int g = 0; g < s.nkv; ++g) {
       for (int i = 0; i < s.npg; ++i) {
         std::vector<std::pair<int, int>> w;
         if (prev_c >= 0) w.push_back({prev_c, prev_n});
         const int b = g * s.gunits + lo(s.gunits, s.npg, i), e = g * s.gunits + lo(s.gunits, s.npg, i + 1);
-        add(AMK_OP_QKV, l, cu_of(g * s.npg + i, n_qkv), b, e, g, w, c_qkv0 + g, shortv ? c_done : -1);
+        add(AMK_OP_QKV, l, cu_of(g * s.npg + i, n_qkv), b, e, g, w, tinyv ? c_qkv0 : c_qkv0 + g,
+            shortv ? c_done : -1);
       }
     }
     bump(n_qkv);
+    if (tinyv) {
+      // O tasks compute the attention themselves from q and the KV cache
+      const int n = n_tasks(s.H, 1);
+      const int sig = n_ctr++;
+      for (int i = 0; i < n; ++i)
+        add(AMK_OP_O, l, cu_of(i, n), lo(s.H, n, i), lo(s.H, n, i + 1), 1, {{c_qkv0, n_qkv}}, sig);
+      bump(n);
+      auto gu = stage(AMK_OP_GATEUP, l, s.I, 2, sig, n);
+      auto dn = stage(AMK_OP_DOWN, l, s.H, 1, gu.first, gu.second);
+      prev_c = dn.first; prev_n = dn.second;
+      continue;
+    }
     if (shortv) {
       // the QKV task of group g that finishes last runs the group's attention
       for (int g = 0; g < s.nkv; ++g)
@@ -267,6 +286,7 @@ struct BufIds {
   int count() const { return 7 * L + 4; }
   bool is_kv(int b) const { return b >= 3 * L + 1 && b < 4 * L + 1; }
   bool is_part(int b) const { return b >= 4 * L + 1 && b < 5 * L + 1; }
+  bool is_o(int b) const { return b >= 5 * L + 1 && b < 6 * L + 1; }
 };
 
 void accesses(const Shape& s, const BufIds& ids, const amk_task_t& t, std::vector<Access>* rd,
@@ -308,7 +328,12 @@ void accesses(const Shape& s, const BufIds& ids, const amk_task_t& t, std::vecto
       break;
     }
     case AMK_OP_O:
-      rd->push_back({ids.o(l), 0, s.nq * s.hd});
+      if (t.aux == 1) {  // attention computed in the task from q and the whole KV stage of the layer
+        rd->push_back({ids.q(l), 0, s.q_units});
+        rd->push_back({ids.kv(l), 0, 2 * s.nkv * s.half});
+      } else {
+        rd->push_back({ids.o(l), 0, s.nq * s.hd});
+      }
       rd->push_back({ids.x(2 * l), t.begin, t.end});
       wr->push_back({ids.x(2 * l + 1), t.begin, t.end});
       break;
@@ -402,6 +427,8 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
     if (t.op == AMK_OP_QKV && (t.aux < 0 || t.aux >= s.nkv || t.begin / s.gunits != t.aux ||
                                (t.end - 1) / s.gunits != t.aux))
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: QKV units must lie in KV group aux %ld", i, t.aux);
+    if (t.op == AMK_OP_O && (t.aux < 0 || t.aux > 1))
+      return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: O aux %ld must be 0 or 1", i, t.aux);
     if (t.op == AMK_OP_ARGMAX && (t.begin != 0 || t.end != n_lm))
       return R.fail(AMK_CHECK_WELL_FORMED, i, -1, "task %ld: argmax must reduce all %ld partial slots", i, n_lm);
     if (t.op == AMK_OP_LMHEAD && (t.aux < 0 || t.aux >= n_lm))
@@ -592,7 +619,7 @@ bool check_schedule(const Shape& s, int n_cu, const amk_task_t* tasks, int n, in
       if (!v.empty()) return R.fail(AMK_CHECK_OUTPUT, v[0].task, -1, "task %ld writes the embedding input", v[0].task);
       continue;
     }
-    if (ids.is_part(b) && v.empty() && !read_any[b]) continue;
+    if ((ids.is_part(b) || ids.is_o(b)) && v.empty() && !read_any[b]) continue;
     std::sort(v.begin(), v.end(), [](const W& a, const W& c) { return a.lo < c.lo; });
     int at = 0;
     for (auto& w : v) {

@@ -29,6 +29,7 @@ struct Shape {
   int nsplit = 0;        // attention position splits per KV head (long schedule)
   int max_jobs = 0;      // GEMV rows per task cap
   int short_context = 0; // steps with pos + 1 <= short_context use the short schedule
+  int tiny_context = 0;  // steps with pos + 1 <= tiny_context use the tiny schedule
   float theta = 0.f, eps = 0.f;
 };
 
@@ -49,8 +50,12 @@ struct Schedule {
   int n_lm_slots = 0;              // argmax partial slots (one per LM-head task)
 };
 
-// Default of amk_tuning_t.short_context.
+// Defaults of amk_tuning_t.short_context and .tiny_context (measured crossovers
+// on the 8B shape: the tiny schedule gains about 140 us at pos 0 and breaks
+// even near pos 6, where its per-task attention catches up with the saved
+// stage).
 constexpr int kDefaultShortContext = 256;
+constexpr int kDefaultTinyContext = 6;
 
 // Deterministic lowering of one decode step onto n_cu queues, schedule
 // variant AMK_SCHEDULE_SHORT or AMK_SCHEDULE_LONG.

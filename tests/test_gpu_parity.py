@@ -30,9 +30,12 @@ LONG_ALWAYS = -1
 
 
 def tuning_for(amk, variant=None, **kw):
-    sc = {None: 0, "short": SHORT_ALWAYS, "long": LONG_ALWAYS}[variant]
+    """variant None: the step picks by position; 'tiny' / 'short' / 'long' force one
+    (tiny needs pos < AMK_TINY_MAX)."""
+    sc = {None: 0, "tiny": 0, "short": SHORT_ALWAYS, "long": LONG_ALWAYS}[variant]
+    tc = {None: 0, "tiny": amk.AMK_TINY_MAX}.get(variant, -1)
     return amk.amk_tuning_t(kw.get("attn_splits", 0), kw.get("timeout_us", 0), kw.get("max_rows", 0),
-                            kw.get("trace", 0), sc)
+                            kw.get("trace", 0), sc, tc)
 
 
 def say(msg):
@@ -152,6 +155,20 @@ def test_tiny_filled_cache(amk, torch_cuda, fmt, pos, variant):
 
 
 @pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("pos", [0, 1, 6, 7])
+def test_tiny_schedule_positions(amk, torch_cuda, fmt, pos):
+    """The tiny schedule (every O task computes all heads' attention itself)
+    at the positions it serves, against the oracle and the short schedule."""
+    w = weights_for("tiny")
+    cfg = w.cfg
+    kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=64)
+    o = oracle_decode(w, fmt, pos, 1, kv)
+    for variant in ("tiny", "short"):
+        g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3], tuning=tuning_for(amk, variant))
+        compare(f"tiny {variant}", fmt, g, o, pos)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
 def test_tiny_attention_split_counts(amk, torch_cuda, fmt):
     """The same step under several attention split counts (1 split .. 64)."""
     w = weights_for("tiny")
@@ -212,26 +229,26 @@ def test_8b_positions(amk, torch_cuda, fmt):
     for pos in cfg.positions:
         kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=pos + 2)
         o = oracle_decode(w, fmt, pos, 1, kv)
-        for variant in ("short", "long"):
+        for variant in ("short", "long") + (("tiny",) if pos < amk.AMK_TINY_MAX else ()):
             g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3], tuning=tuning_for(amk, variant))
             compare(f"llama3_8b {variant}", fmt, g, o, pos)
 
 
-@pytest.mark.parametrize("variant", ["short", "long"])
+@pytest.mark.parametrize("variant", ["short", "long", "tiny"])
 def test_trace_records(amk, torch_cuda, variant):
     """Per-task device timestamps are ordered within each task, every task
     ran, and exactly one task per (layer, KV group) ran its inline task."""
     import torch
     w = weights_for("tiny")
     cfg = w.cfg
-    pos = 100
+    pos = 5 if variant == "tiny" else 100
     kv_np = synth.make_kv_cache(cfg, pos, seed=1, max_seq=256)
     tuning = tuning_for(amk, variant, trace=1)
     dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", 256)), weights_to_device(w, "bf16"), tuning)
     kv = kv_to_device(kv_np)
     logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
     dec.step(1, pos, kv, logits)
-    want = amk.AMK_SCHEDULE_SHORT if variant == "short" else amk.AMK_SCHEDULE_LONG
+    want = {"short": amk.AMK_SCHEDULE_SHORT, "long": amk.AMK_SCHEDULE_LONG, "tiny": amk.AMK_SCHEDULE_TINY}[variant]
     tasks, _ = amk.amk_schedule_export(dec.cfg, torch.cuda.get_device_properties(0).multi_processor_count,
                                        tuning, variant=want)
     got, tr = amk.amk_trace_copy(dec.handle, len(tasks))
@@ -249,6 +266,9 @@ def test_trace_records(amk, torch_cuda, variant):
             key = (t.layer, t.aux)
             assert key not in chained
             chained[key] = t.op
+    if variant == "tiny":
+        assert not chained
+        return
     assert sorted(chained) == [(l, g) for l in range(cfg.n_layers) for g in range(cfg.n_kv_heads)]
     assert set(chained.values()) == {amk.AMK_OP_QKV if variant == "short" else amk.AMK_OP_ATTN}
 

@@ -59,7 +59,7 @@ def producers(tasks, c):
 
 @pytest.mark.parametrize("name", list(synth.CONFIGS))
 @pytest.mark.parametrize("n_cu", [256, 13])
-@pytest.mark.parametrize("variant", [amk.AMK_SCHEDULE_SHORT, amk.AMK_SCHEDULE_LONG])
+@pytest.mark.parametrize("variant", [amk.AMK_SCHEDULE_SHORT, amk.AMK_SCHEDULE_LONG, amk.AMK_SCHEDULE_TINY])
 def test_real_lowering_accepted(lib, name, n_cu, variant):
     cfg = cfg_of(name, "w8a16")
     tasks, nc = amk.amk_schedule_export(cfg, n_cu, variant=variant)
@@ -69,6 +69,7 @@ def test_real_lowering_accepted(lib, name, n_cu, variant):
     seen = {}
     for t in tasks:
         if t.cu == amk.AMK_CU_INLINE:
+            assert variant != amk.AMK_SCHEDULE_TINY
             assert t.op == (amk.AMK_OP_ATTN if variant == amk.AMK_SCHEDULE_SHORT else amk.AMK_OP_COMBINE)
             continue
         seen.setdefault(t.cu, []).append(t.seq)
@@ -409,3 +410,45 @@ def test_short_producer_count_mismatch_rejected(tiny_short):
     m[g1].wait_count[0] -= 1
     rep = check(cfg, m, nc)
     assert not rep.ok, rep.message
+
+
+# ------------------------------------------------------------------ tiny schedule (attention in the O tasks)
+def test_schedule_shape_8b_tiny(lib):
+    cfg = cfg_of("llama3_8b")
+    tasks, nc = amk.amk_schedule_export(cfg, 256, variant=amk.AMK_SCHEDULE_TINY)
+    assert check(cfg, tasks, nc, 256).ok
+    assert not [t for t in tasks if t.op in (amk.AMK_OP_ATTN, amk.AMK_OP_COMBINE) or t.cu == amk.AMK_CU_INLINE]
+    qkv = [t for t in tasks if t.op == amk.AMK_OP_QKV and t.layer == 7]
+    o = [t for t in tasks if t.op == amk.AMK_OP_O and t.layer == 7]
+    assert len({t.signal_counter for t in qkv}) == 1 and all(t.chain_counter == -1 for t in qkv)
+    assert all(t.aux == 1 and t.n_wait == 1 and t.wait_counter[0] == qkv[0].signal_counter and
+               t.wait_count[0] == len(qkv) for t in o)
+
+
+@pytest.fixture(scope="module")
+def tiny_tiny(lib):
+    cfg = cfg_of("tiny")
+    tasks, nc = amk.amk_schedule_export(cfg, N_CU, variant=amk.AMK_SCHEDULE_TINY)
+    assert check(cfg, tasks, nc).ok
+    return cfg, tasks, nc
+
+
+def test_tiny_o_without_wait_rejected(tiny_tiny):
+    """An O task that computes attention from q and the KV cache must be
+    ordered after every QKV task: without its wait it reads the new K/V row
+    before it is appended."""
+    cfg, tasks, nc = tiny_tiny
+    m = clone(tasks)
+    m[find(m, amk.AMK_OP_O, 2)].n_wait = 0
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule in (amk.AMK_CHECK_KV_ORDER, amk.AMK_CHECK_RACE), rep.message
+
+
+def test_tiny_o_reading_unwritten_output_rejected(tiny_tiny):
+    """In the tiny schedule nobody writes the attention output buffer: an O
+    task that reads it (aux 0) reads a region no task writes."""
+    cfg, tasks, nc = tiny_tiny
+    m = clone(tasks)
+    m[find(m, amk.AMK_OP_O, 1)].aux = 0
+    rep = check(cfg, m, nc)
+    assert not rep.ok and rep.rule == amk.AMK_CHECK_OUTPUT, rep.message
