@@ -140,10 +140,13 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
  * 0..pos-1 and appends position pos (all layers), writes all `vocab` logits
  * and the greedy next token (lowest index among equal maxima) into the
  * handle's device slot (amk_next_token_ptr).
- *   kv_cache: device pointer, bf16 [n_layers][2 (K, V)][n_kv_heads][max_seq][head_dim]
- *   logits:   device pointer, fp32 [vocab]
- * Errors: AMK_ERR_INVALID_ARGUMENT for token outside [0, vocab) or pos outside
- * [0, max_seq); a sticky device error of an earlier step (AMK_ERR_TIMEOUT /
+ *   kv_cache: device pointer, 256-byte aligned, bf16
+ *             [n_layers][2 (K, V)][n_kv_heads][max_seq][head_dim]
+ *             (every row then fills whole cache lines: rows appended by this
+ *             step never share a line with rows another workgroup reads)
+ *   logits:   device pointer, 16-byte aligned, fp32 [vocab]
+ * Errors: AMK_ERR_INVALID_ARGUMENT for token outside [0, vocab), pos outside
+ * [0, max_seq) or a misaligned pointer; a sticky device error of an earlier step (AMK_ERR_TIMEOUT /
  * AMK_ERR_ABORTED, visible once that step finished) is returned and nothing
  * is launched until amk_reset().  One handle must not be driven from two
  * streams at once. */

@@ -287,11 +287,15 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     auto take = [&](size_t bytes) { Region r{top, bytes}; top = round_up(top + bytes, 256); return r; };
     const Region r_layers = take(sizeof(DevLayer) * L);
     const Region r_rope = take(sizeof(float) * 2 * (size_t)s.max_seq * s.half);
-    const Region r_x = take(sizeof(float) * (size_t)(2 * L + 1) * s.H);
-    const Region r_q = take(sizeof(float) * (size_t)L * s.nq * s.hd);
-    const Region r_part = take(sizeof(float) * (size_t)L * s.nkv * s.nsplit * rec);
-    const Region r_o = take(sizeof(float) * (size_t)L * s.nq * s.hd);
-    const Region r_a = take(sizeof(float) * (size_t)L * s.I);
+    // vectors of the residual stream and per-layer activations on separate
+    // 256-byte boundaries (64 floats)
+    const int xs = (int)round_up(s.H, 64), qs = (int)round_up((size_t)s.nq * s.hd, 64);
+    const int as = (int)round_up(s.I, 64), ps = (int)round_up((size_t)s.nkv * s.nsplit * rec, 64);
+    const Region r_x = take(sizeof(float) * (size_t)(2 * L + 1) * xs);
+    const Region r_q = take(sizeof(float) * (size_t)L * qs);
+    const Region r_part = take(sizeof(float) * (size_t)L * ps);
+    const Region r_o = take(sizeof(float) * (size_t)L * qs);
+    const Region r_a = take(sizeof(float) * (size_t)L * as);
     const Region r_argp = take(sizeof(float) * 2 * n_lm);
     const Region r_next = take(sizeof(int32_t));
     const Region r_abort = take(sizeof(int32_t));
@@ -389,6 +393,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.part = (float*)(base + r_part.off);
     m.o = (float*)(base + r_o.off);
     m.a = (float*)(base + r_a.off);
+    m.xs = xs; m.qs = qs; m.as = as; m.ps = ps;
     m.argp = (float*)(base + r_argp.off);
     m.next_token = (int32_t*)(base + r_next.off);
     m.counters = nullptr;  // per launch: the variant's counters
@@ -423,7 +428,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
 int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, float* logits, void* stream) {
   if (!h || !kv_cache || !logits) return AMK_ERR_INVALID_ARGUMENT;
   if (token < 0 || token >= h->s.V || pos < 0 || pos >= h->s.max_seq) return AMK_ERR_INVALID_ARGUMENT;
-  if (!aligned16(kv_cache) || !aligned16(logits)) return AMK_ERR_INVALID_ARGUMENT;
+  if (((uintptr_t)kv_cache & 255u) != 0 || !aligned16(logits)) return AMK_ERR_INVALID_ARGUMENT;
   const int sticky = *(volatile int32_t*)h->h_status;
   if (sticky != 0) return sticky;
   DeviceGuard guard(h->device);

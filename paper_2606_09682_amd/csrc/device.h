@@ -44,11 +44,16 @@ struct DevModel {
   const DevLayer* layers;    // device array [L]
   // handle-owned tables and scratch
   const float2* rope;        // [max_seq][half] (cos, sin), computed in fp64 on the host
-  float* x;                  // residual stream [2L + 1][H]; slot 0 unused (embedding row is read directly)
-  float* q;                  // [L][nq * hd] roped queries
-  float* part;               // [L][nkv][nsplit][group][kPartHead + hd]
-  float* o;                  // [L][nq * hd] attention output
-  float* a;                  // [L][I] SwiGLU output
+  // Every vector below is written at most once per launch and read only after
+  // its producers' counter; each starts on its own 256-byte boundary (the
+  // strides xs, qs, as, ps, in floats), so no cache line holds values of two
+  // vectors, which the acquire without a cache invalidation relies on.
+  float* x;                  // residual stream [2L + 1][xs]; slot 0 unused (embedding row is read directly)
+  float* q;                  // [L][qs] roped queries (nq * hd used)
+  float* part;               // [L][ps] records [nkv][nsplit][group][kPartHead + hd]
+  float* o;                  // [L][qs] attention output (nq * hd used)
+  float* a;                  // [L][as] SwiGLU output (I used)
+  int32_t xs, qs, as, ps;
   float* argp;               // [n_lm][2] (max logit, index as float bits)
   int32_t* next_token;       // [1]
   uint32_t* counters;        // [n_counters * kCounterStride]

@@ -405,6 +405,22 @@ __device__ __forceinline__ void consume_block(const uint4 (&buf)[N], int& j, int
 }
 
 // ---------------------------------------------------------------- sync wave: counters
+// Acquire after a counter poll.  The polls are agent-coherent loads; what they
+// order is then read with plain loads, with no cache invalidation:
+//  - every vector another workgroup reads (residual stream, q, attention
+//    records and output, SwiGLU output, argmax partials, the KV row at pos) is
+//    written at most once per launch, and read only after all its producers
+//    signalled;
+//  - the launch's own acquire has invalidated every cached copy of earlier
+//    launches' data;
+//  - no cache line holds parts of two such vectors (256-byte strides).
+// So a line a workgroup finds in its L1 or its XCD's L2 was fetched after the
+// producers had released all of it, and the XCD's L2 serves one fetch of an
+// input vector to all its CUs instead of one per CU.  The fence only keeps
+// the compiler from moving those loads above the poll; the hardware issues
+// them after it, since leaving the poll loop depends on the loaded value.
+__device__ __forceinline__ void acquire_after_poll() { __atomic_signal_fence(__ATOMIC_SEQ_CST); }
+
 __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t, const amk_task_t* tp, uint32_t epoch,
                                           uint64_t deadline, int lane, uint64_t* tr) {
   const int nw = t.n_wait;
@@ -441,7 +457,7 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
     __builtin_amdgcn_s_sleep(1);
   }
   if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SATISFIED, (uint64_t)wall_clock64());
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  acquire_after_poll();
   return true;
 }
 
@@ -527,16 +543,16 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
   switch (op) {
     case AMK_OP_QKV:
       if (t.layer == 0) src_bf = m.embed + (size_t)token * m.H;
-      else src = m.x + (size_t)(2 * t.layer) * m.H;
+      else src = m.x + (size_t)(2 * t.layer) * m.xs;
       gain = ldc<const uint16_t*>(&m.layers[t.layer].attn_norm);
       break;
     case AMK_OP_GATEUP:
-      src = m.x + (size_t)(2 * t.layer + 1) * m.H;
+      src = m.x + (size_t)(2 * t.layer + 1) * m.xs;
       gain = ldc<const uint16_t*>(&m.layers[t.layer].mlp_norm);
       break;
-    case AMK_OP_LMHEAD: src = m.x + (size_t)(2 * m.L) * m.H; gain = m.final_norm; break;
-    case AMK_OP_O: src = m.o + (size_t)t.layer * m.nq * m.hd; break;
-    case AMK_OP_DOWN: src = m.a + (size_t)t.layer * m.I; break;
+    case AMK_OP_LMHEAD: src = m.x + (size_t)(2 * m.L) * m.xs; gain = m.final_norm; break;
+    case AMK_OP_O: src = m.o + (size_t)t.layer * m.qs; break;
+    case AMK_OP_DOWN: src = m.a + (size_t)t.layer * m.as; break;
     default: return;
   }
   const int K = task_k(m, t);
@@ -634,7 +650,7 @@ __device__ __forceinline__ void epi_qkv(const DevModel& m, const amk_task_t& t, 
       y1 = b;
     }
     if (mat == W_Q) {
-      float* qd = m.q + (size_t)l * m.nq * m.hd + (size_t)head * m.hd;
+      float* qd = m.q + (size_t)l * m.qs + (size_t)head * m.hd;
       stc(qd + i, y0);
       stc(qd + i + m.half, y1);
     } else {
@@ -656,9 +672,9 @@ __device__ __forceinline__ void epi_residual(const DevModel& m, const amk_task_t
   for (int r = t.begin + lane; r < t.end; r += 64) {
     float y = row_sum(L.part, m.part_stride, g, wr, r - t.begin);
     if (g.int8) y *= L.stat[r - t.begin];
-    const float x = cached ? L.res[r - t.begin] : ldg<float>(m.x + (size_t)xin * m.H + r);
+    const float x = cached ? L.res[r - t.begin] : ldg<float>(m.x + (size_t)xin * m.xs + r);
     const float o = x + y;
-    stc(m.x + (size_t)(xin + 1) * m.H + r, o);
+    stc(m.x + (size_t)(xin + 1) * m.xs + r, o);
     L.res[r - t.begin] = o;
   }
   if (lane == 0) {
@@ -680,7 +696,7 @@ __device__ __forceinline__ void epi_gateup(const DevModel& m, const amk_task_t& 
       uv *= L.stat[j + 1];
     }
     const float silu = gv / (1.0f + __expf(-gv));
-    stc(m.a + (size_t)t.layer * m.I + r, silu * uv);
+    stc(m.a + (size_t)t.layer * m.as + r, silu * uv);
   }
 }
 
@@ -815,7 +831,7 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     }
     if (p0 == 0) {
       // the group's roped queries into LDS while the first rows are in flight
-      const float* qsrc = m.q + ((size_t)layer * m.nq + (size_t)g * G) * HD;
+      const float* qsrc = m.q + (size_t)layer * m.qs + (size_t)g * G * HD;
       for (int i = threadIdx.x; i < G * HD / 4; i += NT)
         *reinterpret_cast<float4*>(qs + 4 * i) = ldg<float4>(qsrc + 4 * i);
       __syncthreads();
@@ -956,7 +972,7 @@ __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int 
     for (int i = 0; i < HR; ++i) {
       const int h = min(h0 + i, m.nq - 1);
       const int g = h / m.group;
-      const float* qh = m.q + ((size_t)layer * m.nq + h) * HD + lane * DPL;
+      const float* qh = m.q + (size_t)layer * m.qs + (size_t)h * HD + lane * DPL;
       const uint16_t* Kp = kv + ((size_t)(layer * 2) * m.nkv + g) * hs + lane * DPL;
       const uint16_t* Vp = kv + ((size_t)(layer * 2 + 1) * m.nkv + g) * hs + lane * DPL;
       if constexpr (DPL == 2) {
@@ -1026,7 +1042,7 @@ __device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g
                                              int lane) {
   const int G = m.group;
   const int rec = G * (kPartHead + HD);
-  const float* base = m.part + ((size_t)(layer * m.nkv + g) * m.nsplit) * rec;
+  const float* base = m.part + (size_t)layer * m.ps + (size_t)g * m.nsplit * rec;
   float* wts = scr;                                        // [GM][64]
   float4* red = reinterpret_cast<float4*>(scr + GM * 64);  // [SP][E4]
   if (wave < G) {
@@ -1075,7 +1091,7 @@ __device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g
       const float4 v = red[k * E4 + t];
       o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
     }
-    float* od = m.o + ((size_t)layer * m.nq + (size_t)g * G) * HD + 4 * t;
+    float* od = m.o + (size_t)layer * m.qs + (size_t)g * G * HD + 4 * t;
     stc(od, o.x); stc(od + 1, o.y); stc(od + 2, o.z); stc(od + 3, o.w);
   }
 }
@@ -1191,8 +1207,8 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
       // one split: the normalised output directly; several: a partial record
       const int j0 = t.begin * chunk, j1 = min(pos + 1, j0 + chunk);
       const int rec = m.group * (kPartHead + HD);
-      float* dst = active == 1 ? m.o + ((size_t)t.layer * m.nq + (size_t)t.aux * m.group) * HD
-                               : m.part + (((size_t)t.layer * m.nkv + t.aux) * m.nsplit + t.begin) * rec;
+      float* dst = active == 1 ? m.o + (size_t)t.layer * m.qs + (size_t)t.aux * m.group * HD
+                               : m.part + (size_t)t.layer * m.ps + ((size_t)t.aux * m.nsplit + t.begin) * rec;
       attention<HD, GM>(m, t.layer, t.aux, j0, j1, kv, L.act, L.part, dst, active > 1, wave, lane);
       drain_vmem();
     }
@@ -1216,7 +1232,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         // task's group has npg producers, an attention split's nsplit
         const uint32_t producers = t.op == AMK_OP_QKV ? (uint32_t)m.npg : (uint32_t)m.nsplit;
         cont = release_signal_last(m, t.signal_counter, epoch * producers, lane);
-        if (cont) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        if (cont) acquire_after_poll();
       } else {
         release_signal(m, t.signal_counter, lane);
       }
@@ -1228,7 +1244,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     // ---- inline task of the chain counter (all waves)
     if (ctl.cont) {
       if (t.op == AMK_OP_QKV) {
-        float* dst = m.o + ((size_t)t.layer * m.nq + (size_t)t.aux * m.group) * HD;
+        float* dst = m.o + (size_t)t.layer * m.qs + (size_t)t.aux * m.group * HD;
         attention<HD, GM>(m, t.layer, t.aux, 0, pos + 1, kv, L.act, L.part, dst, false, wave, lane);
       } else if (active > 1) {
         merge_splits<HD, GM>(m, t.layer, t.aux, active, L.part, wave, lane);

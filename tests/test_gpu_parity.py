@@ -284,6 +284,13 @@ def test_invalid_arguments(amk, torch_cuda):
         with pytest.raises(amk.AmkError) as e:
             dec.step(tok, pos, kv, logits)
         assert e.value.status == amk.AMK_ERR_INVALID_ARGUMENT
+    # a KV cache 16 but not 256 bytes aligned is refused on the host, before any launch
+    n = kv.numel()
+    kv_big = torch.zeros(n + 128, dtype=torch.int16, device="cuda")
+    assert kv_big.data_ptr() % 256 == 0
+    with pytest.raises(amk.AmkError) as e:
+        dec.step(1, 0, kv_big[8:8 + n], logits)
+    assert e.value.status == amk.AMK_ERR_INVALID_ARGUMENT
     dec.step(1, 15, kv, logits)  # last valid position
     assert dec.status() == amk.AMK_OK
     dec.close()
