@@ -302,7 +302,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     const bool tracing = tuning && tuning->trace;
     Region r_tasks[kVariants], r_queue[kVariants], r_trace[kVariants], r_ctr[kVariants];
     for (int v = 0; v < kVariants; ++v) {
-      r_ctr[v] = take(sizeof(uint32_t) * amk::kCounterStride * (size_t)h->sch[v].n_counters);
+      r_ctr[v] = take(sizeof(uint32_t) * amk::kCounterStride * amk::kCounterReplicas * (size_t)h->sch[v].n_counters);
       r_tasks[v] = take(sizeof(amk_task_t) * h->sch[v].tasks.size());
       r_queue[v] = take(sizeof(int32_t) * h->sch[v].queue_start.size());
       r_trace[v] = take(tracing ? sizeof(uint64_t) * AMK_TRACE_FIELDS * h->sch[v].tasks.size() : 0);

@@ -18,8 +18,14 @@ struct DevLayer {
   const uint16_t* mlp_norm;    // bf16 [H]
 };
 
-// Counters live on separate 128-byte lines.
+// Counters live on separate 128-byte lines, each in kCounterReplicas copies
+// (counter c, copy r at element (c * kCounterReplicas + r) * kCounterStride):
+// a producer increments every copy, and workgroup b polls copy b % 16, so a
+// line has 16 pollers (half an XCD) instead of the whole grid's 256.  With
+// one line per counter the polls queue at that line's memory channel and
+// delay the producers' increments (8B bf16: 160 us per step).
 constexpr int kCounterStride = 32;  // uint32 elements
+constexpr int kCounterReplicas = 16;
 
 // Layout of one attention partial record for a (layer, kv head, split):
 // for each of the `group` query heads: [m, l, pad, pad, acc[head_dim]].
@@ -56,7 +62,7 @@ struct DevModel {
   int32_t xs, qs, as, ps;
   float* argp;               // [n_lm][2] (max logit, index as float bits)
   int32_t* next_token;       // [1]
-  uint32_t* counters;        // [n_counters * kCounterStride]
+  uint32_t* counters;        // [n_counters * kCounterReplicas * kCounterStride]
   int32_t* dev_abort;        // device word: nonzero stops every workgroup at its next wait
   int32_t* host_status;      // host-mapped: first device error code
   const int32_t* host_abort; // host-mapped: raised by amk_set_abort

@@ -428,7 +428,8 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
   uint32_t* p = nullptr;
   uint32_t target = 0;
   if (lane < nw) {
-    p = m.counters + (size_t)ldg<int32_t>(&tp->wait_counter[lane]) * kCounterStride;
+    p = m.counters + ((size_t)ldg<int32_t>(&tp->wait_counter[lane]) * kCounterReplicas +
+                      blockIdx.x % kCounterReplicas) * kCounterStride;
     target = epoch * (uint32_t)ldg<int32_t>(&tp->wait_count[lane]);
   }
   uint32_t spins = 0;
@@ -463,9 +464,9 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
 
 __device__ __forceinline__ void release_signal(const DevModel& m, int counter, int lane) {
   drain_vmem();  // every published store of this wave is coherent at agent scope
-  if (lane == 0 && counter >= 0)
-    __hip_atomic_fetch_add(m.counters + (size_t)counter * kCounterStride, 1u, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+  if (lane < kCounterReplicas && counter >= 0)
+    __hip_atomic_fetch_add(m.counters + ((size_t)counter * kCounterReplicas + lane) * kCounterStride, 1u,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Release, increment `counter`, and report whether this increment brought it
@@ -474,9 +475,10 @@ __device__ __forceinline__ void release_signal(const DevModel& m, int counter, i
 __device__ __forceinline__ bool release_signal_last(const DevModel& m, int counter, uint32_t target, int lane) {
   drain_vmem();
   uint32_t old = 0;
-  if (lane == 0)
-    old = __hip_atomic_fetch_add(m.counters + (size_t)counter * kCounterStride, 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
+  // copy 0's return value orders the producers
+  if (lane < kCounterReplicas)
+    old = __hip_atomic_fetch_add(m.counters + ((size_t)counter * kCounterReplicas + lane) * kCounterStride, 1u,
+                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   old = (uint32_t)__builtin_amdgcn_readfirstlane((int)old);
   return (int32_t)(old + 1u - target) == 0;
 }
