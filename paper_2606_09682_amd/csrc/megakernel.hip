@@ -774,10 +774,6 @@ __device__ __forceinline__ RowVec<EPL> load_row(const uint16_t* p) {
   return r;
 }
 template <int EPL>
-__device__ __forceinline__ void zero_row(RowVec<EPL>& r) {
-  if constexpr (EPL == 8) r.v = make_uint4(0, 0, 0, 0); else r.v = make_uint2(0, 0);
-}
-template <int EPL>
 __device__ __forceinline__ float row_elem(const RowVec<EPL>& r, int e) {
   uint32_t w;
   if constexpr (EPL == 8) w = (e < 2) ? r.v.x : (e < 4) ? r.v.y : (e < 6) ? r.v.z : r.v.w;
@@ -818,26 +814,32 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     for (int e = 0; e < EPL; ++e) acc[h][e] = 0.f;
   }
 
+  // the group's roped queries (G * HD / 4 <= NT float4s) into LDS first: the
+  // threads that move them do so before issuing their rows, so the queries
+  // do not wait behind the K / V stream
+  static_assert(GM * HD / 4 <= NT, "one query vector per thread");
+  if ((int)threadIdx.x < G * HD / 4) {
+    const float* qsrc = m.q + (size_t)layer * m.qs + (size_t)g * G * HD;
+    *reinterpret_cast<float4*>(qs + 4 * threadIdx.x) = ldg<float4>(qsrc + 4 * threadIdx.x);
+  }
   for (int p0 = 0; p0 < n; p0 += RP) {
-    // rows of this lane: r_k = p0 + (k * NW + wave) * RPW + sub
+    // rows of this lane: r_k = p0 + (k * NW + wave) * RPW + sub.  Every load
+    // is issued (rows past the range re-read its first row, whose score is
+    // masked to -inf, so it weighs 0): the compiler then waits for each row
+    // alone instead of the whole batch.
     RowVec<EPL> kr[KB], vr[KB];
 #pragma unroll
     for (int k = 0; k < KB; ++k) {
       const int r = p0 + (k * NW + wave) * RPW + sub;
-      zero_row<EPL>(kr[k]);
-      zero_row<EPL>(vr[k]);
       if (r < n) {
         kr[k] = load_row<EPL>(Kp + (size_t)r * HD);
         vr[k] = load_row<EPL>(Vp + (size_t)r * HD);
+      } else {
+        kr[k] = load_row<EPL>(Kp);
+        vr[k] = load_row<EPL>(Vp);
       }
     }
-    if (p0 == 0) {
-      // the group's roped queries into LDS while the first rows are in flight
-      const float* qsrc = m.q + (size_t)layer * m.qs + (size_t)g * G * HD;
-      for (int i = threadIdx.x; i < G * HD / 4; i += NT)
-        *reinterpret_cast<float4*>(qs + 4 * i) = ldg<float4>(qsrc + 4 * i);
-      __syncthreads();
-    }
+    if (p0 == 0) __syncthreads();
     // rows in sub-batches of SB: scores for every query head, then one
     // online-softmax update per head and sub-batch.  The running max / sum
     // belong to the lane's row group (LPR lanes sharing its rows), so no
