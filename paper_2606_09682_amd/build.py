@@ -5,6 +5,7 @@
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -24,6 +25,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", os.path.
           "-Wall", "-Wno-unused-command-line-argument"]
 
 SOURCES = ["megakernel.hip", "schedule.cpp", "api.cpp"]
+# per-kernel register / scratch report of the device code, parsed from the
+# compiler's resource-usage remarks
+RESOURCES = os.path.join(BUILD, "resource_usage.txt")
 
 
 def hipcc() -> str:
@@ -35,11 +39,33 @@ def hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc()] + COMMON + DEVICE_FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if src.endswith(".hip") else []
+    cmd = [hipcc()] + COMMON + DEVICE_FLAGS + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    if extra:
+        _write_resources(r.stderr)
     return obj
+
+
+def _write_resources(remarks: str) -> None:
+    """One line per kernel: name, VGPRs, scratch bytes per lane, spilled VGPRs."""
+    rows, cur = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"remark:\s+(Function Name|VGPRs|ScratchSize \[bytes/lane\]|VGPRs Spill):\s+(\S+)", line)
+        if not m:
+            continue
+        key, val = m.group(1), m.group(2)
+        if key == "Function Name":
+            cur = {"name": val}
+            rows.append(cur)
+        elif cur is not None:
+            cur[key] = val
+    with open(RESOURCES, "w") as f:
+        for r in rows:
+            f.write(f"{r['name']} vgprs={r.get('VGPRs')} scratch={r.get('ScratchSize [bytes/lane]')} "
+                    f"vgpr_spill={r.get('VGPRs Spill')}\n")
 
 
 def build(verbose: bool = False) -> str:

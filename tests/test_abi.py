@@ -158,3 +158,18 @@ def test_null_arguments_fail_cleanly(lib):
     assert lib.amk_reset(None) == amk.AMK_ERR_INVALID_ARGUMENT
     assert lib.amk_destroy(None) == amk.AMK_OK
     assert amk.amk_kv_cache_bytes(amk.amk_config_t()) == 0
+
+
+def test_kernels_use_no_scratch(lib):
+    """Every decode-kernel instantiation keeps its state in registers: no
+    scratch memory and no spilled VGPRs (the build records the compiler's
+    resource-usage remarks)."""
+    from paper_2606_09682_amd import build
+    if not os.path.exists(build.RESOURCES):
+        build.build()
+    rows = [line.split() for line in open(build.RESOURCES) if "amk_decode_kernel" in line]
+    assert len(rows) == 8  # head_dim {64, 128} x group {4, 8} x {bf16, W8A16}
+    for name, *kv in rows:
+        fields = dict(x.split("=") for x in kv)
+        assert fields["scratch"] == "0" and fields["vgpr_spill"] == "0", (name, fields)
+        assert int(fields["vgprs"]) <= 256, (name, fields)
