@@ -617,13 +617,18 @@ __device__ __forceinline__ Ranges wave_ranges(const Gemv& g) {
 }
 
 __device__ __forceinline__ float row_sum(const float* part, int stride, const Gemv& g, const Ranges& wr, int j) {
-  float s = 0.f;
   const int lo = j * g.gpr, hi = lo + g.gpr;
+  // every wave's slot is read (all reads in flight at once), the ones of
+  // waves that wrote nothing for row j are dropped: a wave with an empty
+  // range wrote nothing, even if its start lies inside the row
+  float v[NSW];
+#pragma unroll
+  for (int sw = 0; sw < NSW; ++sw) v[sw] = part[sw * stride + j];
+  float s = 0.f;
 #pragma unroll
   for (int sw = 0; sw < NSW; ++sw) {
     const int gb = wr.b[sw], ge = wr.b[sw + 1];
-    // a wave with an empty range wrote nothing, even if gb lies inside the row
-    if (gb < ge && gb < hi && ge > lo) s += part[sw * stride + j];
+    s += (gb < ge && gb < hi && ge > lo) ? v[sw] : 0.f;
   }
   return s;
 }
