@@ -964,8 +964,8 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
 // into act[h * HD + d]: the input of an O task of the tiny schedule, which
 // computes it itself instead of waiting for an attention stage.  Each wave
 // takes HR heads per round; lane owns head dims [lane * DPL, (lane + 1) * DPL).
-// All q / K / V loads of a round go out before any arithmetic; positions past
-// pos re-read row pos (clamped, unused).
+// All q / K / V loads of a round go out before any arithmetic, once per KV
+// group; positions past pos re-read row pos (clamped, unused).
 template <int HD>
 __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int pos, const uint16_t* __restrict__ kv,
                                               float* __restrict__ act, int wave, int lane) {
@@ -974,6 +974,9 @@ __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int 
   constexpr int T = AMK_TINY_MAX;
   const int n = pos + 1;
   const size_t hs = (size_t)m.max_seq * HD;
+  // the HR heads of a round share one KV group when the group size is a
+  // multiple of HR (heads h0.. h0 + HR - 1 with h0 a multiple of HR)
+  const bool one_group = m.group % HR == 0;
   for (int h0 = wave * HR; h0 < m.nq; h0 += NW * HR) {
     float qv[HR][DPL];
     uint32_t kr[HR][T], vr[HR][T];  // DPL bf16 values per row (the low half only when DPL == 1)
@@ -991,6 +994,9 @@ __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int 
       } else {
         qv[i][0] = ldg<float>(qh);
       }
+      // one load per KV group (the other heads of the group copy it below);
+      // positions past pos re-read row pos (clamped, unused)
+      if (i > 0 && one_group) continue;
 #pragma unroll
       for (int p = 0; p < T; ++p) {
         const size_t off = (size_t)min(p, n - 1) * HD;
@@ -1002,6 +1008,15 @@ __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int 
           vr[i][p] = ldg<uint16_t>(Vp + off);
         }
       }
+    }
+    if (one_group) {
+#pragma unroll
+      for (int i = 1; i < HR; ++i)
+#pragma unroll
+        for (int p = 0; p < T; ++p) {
+          kr[i][p] = kr[0][p];
+          vr[i][p] = vr[0][p];
+        }
     }
 #pragma unroll
     for (int i = 0; i < HR; ++i) {
