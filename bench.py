@@ -9,7 +9,13 @@ oracle before its time is reported.
 
 A step = one amk_decode_step (one cooperative launch: the whole decode hot
 path).  Inputs are resident in HBM before timing starts; the timed region is
-K back-to-back steps bracketed by torch.cuda.synchronize().
+K back-to-back steps bracketed by torch.cuda.synchronize() (default 25
+warm-ups and 100 timed steps; median and p10/p90 of the per-launch times are
+reported too).  Also reported: the whole-token host time including the
+next-token readback, the device's streaming-read peak (amk_read_probe over
+8 GiB), a flag for any time below the bandwidth floor, GPU clocks and power
+from amd-smi when it is present, and the CPU oracle's time per step (median
+of 3) on this host.
 """
 from __future__ import annotations
 
@@ -55,16 +61,65 @@ def counter_traffic(workload: str):
     return float(b.group(1))
 
 
-def blas_threads() -> int:
+def blas_info():
+    """(threads, library) of the BLAS numpy uses here."""
     try:
         from threadpoolctl import threadpool_info
-        info = threadpool_info()
-        return max((i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"), default=1)
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            return max(i.get("num_threads", 1) for i in info), info[0].get("internal_api", "?")
     except Exception:
-        return os.cpu_count() or 1
+        pass
+    return os.cpu_count() or 1, "?"
 
 
-def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True):
+def host_ram_gb():
+    try:
+        import psutil
+        return round(psutil.virtual_memory().total / 2**30, 1)
+    except Exception:
+        return None
+
+
+def smi_snapshot():
+    """GPU clock and power lines from amd-smi, or None when it is absent."""
+    import shutil
+    import subprocess
+    exe = shutil.which("amd-smi")
+    if not exe:
+        return None
+    try:
+        out = subprocess.run([exe, "metric", "-g", "0", "-c", "-p"], capture_output=True, text=True,
+                             timeout=20).stdout
+    except Exception:
+        return None
+    keep = [ln.strip() for ln in out.splitlines()
+            if any(k in ln for k in ("GFX_0", "CLK:", "SOCKET_POWER", "POWER:", "MEM_0"))]
+    return keep[:12] or None
+
+
+def read_peak_gbs(amk, torch, nbytes=8 << 30):
+    """Best streaming-read rate of this device over nbytes (amk_read_probe)."""
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    stream = torch.cuda.current_stream()
+    best = 0.0
+    for blocks in (n_cu, 2 * n_cu, 4 * n_cu, 8 * n_cu):
+        sink = torch.empty(blocks * 512, dtype=torch.int32, device="cuda")
+        for rep in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            amk.amk_read_probe(buf.data_ptr(), nbytes, blocks, sink.data_ptr(), stream.cuda_stream)
+            e1.record(stream)
+            e1.synchronize()
+            if rep:
+                best = max(best, nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del buf
+    torch.cuda.empty_cache()
+    return best
+
+
+def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repeats=1):
     import oracle
     import synth
     from synth.device import config_kwargs, kv_to_device, weights_to_device
@@ -86,10 +141,13 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True):
     if check:
         log(f"variant {fmt} pos {pos}: oracle step")
         model = oracle.OracleModel(w, fmt, np.float32, cache=False)
-        kv_ref = kv_np.copy()
-        t0 = time.perf_counter()
-        ref_logits = oracle.decode_step(model, 1, pos, kv_ref)
-        cpu_s = time.perf_counter() - t0
+        times = []
+        for _ in range(oracle_repeats):
+            kv_ref = kv_np.copy()
+            t0 = time.perf_counter()
+            ref_logits = oracle.decode_step(model, 1, pos, kv_ref)
+            times.append(time.perf_counter() - t0)
+        cpu_s = float(np.median(times))
         ref_tok = oracle.argmax_first(ref_logits)
         err = float(np.max(np.abs(logits.cpu().numpy().astype(np.float64) - ref_logits)))
         res.update(oracle_s=cpu_s, max_abs_logit_err=err, token=tok, oracle_token=ref_tok,
@@ -101,6 +159,7 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True):
     for _ in range(warmup):
         dec.step(1, pos, kv, logits)
     torch.cuda.synchronize()
+    smi_before = smi_snapshot() if check else None
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     t0 = time.perf_counter()
@@ -111,26 +170,39 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     launch_us = np.array([s.elapsed_time(e) * 1e3 for s, e in zip(starts, ends)])
+    smi_after = smi_snapshot() if check else None
+    # whole token as a host sees it: the API call plus the next-token readback
+    n_rb = max(1, min(steps, 20))
+    t0 = time.perf_counter()
+    for _ in range(n_rb):
+        dec.step(1, pos, kv, logits)
+        dec.next_token()
+    token_wall_us = (time.perf_counter() - t0) / n_rb * 1e6
     status = dec.status()
     dec.close()
     del tensors
     torch.cuda.empty_cache()
     nbytes = cfg.algorithmic_bytes(fmt, pos)
     med = float(np.median(launch_us))
-    res.update(status=status, wall_us_per_step=wall / steps * 1e6, launch_us_median=med,
+    res.update(status=status, wall_us_per_step=wall / steps * 1e6, token_wall_us_with_readback=token_wall_us,
+               launch_us_median=med,
                launch_us_mean=float(np.mean(launch_us)), launch_us_p10=float(np.percentile(launch_us, 10)),
                launch_us_p90=float(np.percentile(launch_us, 90)), algorithmic_bytes=nbytes,
                achieved_gbs=nbytes / (float(np.mean(launch_us)) * 1e-6) / 1e9,
                floor_us=nbytes / (PEAK_HBM_GBS * 1e9) * 1e6)
     res["floor_ratio"] = res["launch_us_mean"] / res["floor_us"]
+    # a time below the bandwidth floor would be a measurement artefact
+    res["below_floor"] = bool(float(np.min(launch_us)) < res["floor_us"])
+    if smi_before or smi_after:
+        res["amd_smi"] = {"before": smi_before, "after": smi_after}
     return res
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--config", default="llama3_8b")
     ap.add_argument("--variants", default="all", help="'all' or 'main' (bf16 at position 0 only)")
     ap.add_argument("--no-check", action="store_true", help="skip the oracle gate (profiling runs)")
@@ -176,11 +248,15 @@ def main():
             t0 = time.perf_counter()
             synth.add_w8a16(w)
             log(f"quantised in {time.perf_counter() - t0:.1f}s")
-        results.append(run_variant(amk, torch, w, fmt, pos, args.steps, args.warmup, check=not args.no_check))
+        results.append(run_variant(amk, torch, w, fmt, pos, args.steps, args.warmup, check=not args.no_check,
+                                   oracle_repeats=3 if not results else 1))
         if results[-1].get("correct") is False or results[-1]["status"] != 0:
             log(f"variant {fmt} pos {pos} FAILED its correctness gate: {results[-1]}")
     main_res = results[0]
-    ok = all(r.get("correct") is not False and r["status"] == 0 for r in results)
+    ok = all(r.get("correct") is not False and r["status"] == 0 and not r["below_floor"] for r in results)
+    peak = None if args.no_check else read_peak_gbs(amk, torch)
+    if peak:
+        log(f"streaming-read peak {peak:.0f} GB/s")
     workload = f"{cfg.name}_bf16_pos{cfg.positions[0]}"
     traffic = counter_traffic(workload)
     out = {
@@ -202,14 +278,18 @@ def main():
         "roofline": {"bound": "hbm", "achieved": main_res["achieved_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": main_res["achieved_gbs"] / PEAK_HBM_GBS,
                      "traffic": traffic},
+        "measured_read_peak_gbs": peak,
+        "frac_of_measured_peak": (main_res["achieved_gbs"] / peak) if peak else None,
         "cpu_baseline": None,
         "variants": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in r.items()} for r in results],
     }
     if "oracle_s" in main_res:
-        out["cpu_baseline"] = {"value": main_res["oracle_s"] * 1e6, "unit": "µs/token", "cores": blas_threads(),
+        threads, blas = blas_info()
+        out["cpu_baseline"] = {"value": main_res["oracle_s"] * 1e6, "unit": "µs/token", "cores": threads,
                                "kind": "oracle",
-                               "sample": f"one full decode step of {workload} (numpy fp32, weights decoded "
-                                         f"from bf16 per use)"}
+                               "sample": f"median of 3 full decode steps of {workload} (numpy fp32, weights "
+                                         f"decoded from bf16 per use; BLAS {blas}, {os.cpu_count()} host "
+                                         f"CPUs, {host_ram_gb()} GiB RAM)"}
     print(json.dumps(out), flush=True)
 
 

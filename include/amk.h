@@ -207,6 +207,21 @@ enum {
  * was launched. */
 int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_tasks, int32_t* variant);
 
+/* ---- measurement --------------------------------------------------------- */
+
+/* Streaming-read reference: enqueue on `stream` one read of `bytes` of device
+ * memory at `buf` by `blocks` workgroups of 512 threads (16 bytes per thread
+ * and load, grid-stride, a few loads in flight per thread), each thread
+ * leaving an XOR of what it read in sink[thread] (a device buffer of
+ * blocks * 512 uint32, owned by the caller, so the reads are not optimised
+ * away).  Asynchronous; time it with events on the same stream.  The read
+ * rate of a large buffer is this device's practical HBM peak, which the
+ * decode step's achieved bandwidth is compared with.
+ * Errors: AMK_ERR_INVALID_ARGUMENT for NULL pointers, bytes not a positive
+ * multiple of 16, buf not 16-byte aligned or blocks outside [1, 65536];
+ * AMK_ERR_DEVICE for a launch failure. */
+int amk_read_probe(const void* buf, int64_t bytes, int32_t blocks, uint32_t* sink, void* stream);
+
 /* ---- schedule introspection (CPU only, no device needed) -------------------- */
 
 /* Schedule variants.  All compute the same step; they differ in where the

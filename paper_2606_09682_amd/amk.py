@@ -114,6 +114,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "amk_next_token_ptr": (ctypes.c_void_p, [ctypes.c_void_p]),
         "amk_copy_next_token": (ctypes.c_int, [ctypes.c_void_p, P(ctypes.c_int32), ctypes.c_void_p]),
         "amk_get_status": (ctypes.c_int, [ctypes.c_void_p]),
+        "amk_read_probe": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p]),
         "amk_reset": (ctypes.c_int, [ctypes.c_void_p]),
         "amk_set_abort": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
         "amk_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -176,6 +178,11 @@ def amk_copy_next_token(h, stream: int = 0) -> int:
 
 def amk_get_status(h) -> int:
     return int(load().amk_get_status(h))
+
+
+def amk_read_probe(buf_ptr: int, nbytes: int, blocks: int, sink_ptr: int, stream: int) -> None:
+    """Enqueue one streaming read of nbytes at device address buf_ptr (see amk.h)."""
+    _check(load().amk_read_probe(buf_ptr, nbytes, blocks, sink_ptr, stream), "amk_read_probe")
 
 
 def amk_reset(h) -> None:

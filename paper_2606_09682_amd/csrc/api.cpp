@@ -22,6 +22,7 @@ using amk::amk_internal_attn_scratch;
 using amk::amk_internal_launch;
 using amk::amk_internal_occupancy;
 using amk::amk_internal_prepare;
+using amk::amk_internal_read_probe;
 using amk::amk_internal_threads;
 
 constexpr int kVariants = 3;
@@ -462,6 +463,12 @@ int amk_copy_next_token(amk_handle_t h, int32_t* dst, void* stream) {
       hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
     return AMK_ERR_DEVICE;
   return AMK_OK;
+}
+
+int amk_read_probe(const void* buf, int64_t bytes, int32_t blocks, uint32_t* sink, void* stream) {
+  if (!buf || !sink || bytes <= 0 || bytes % 16 || !aligned16(buf) || blocks < 1 || blocks > 65536)
+    return AMK_ERR_INVALID_ARGUMENT;
+  return amk_internal_read_probe(buf, bytes, blocks, sink, stream);
 }
 
 int amk_get_status(amk_handle_t h) {

@@ -86,5 +86,6 @@ extern "C" int amk_internal_threads(void);
 extern "C" int amk_internal_attn_scratch(int group, int head_dim);
 extern "C" int amk_internal_prepare(int head_dim, int group, int fmt, int lds_bytes);
 extern "C" int amk_internal_occupancy(int head_dim, int group, int fmt, int lds_bytes, int* blocks_per_cu);
+extern "C" int amk_internal_read_probe(const void* buf, int64_t bytes, int32_t blocks, uint32_t* sink, void* stream);
 
 }  // namespace amk

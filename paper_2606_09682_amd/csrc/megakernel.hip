@@ -1289,6 +1289,32 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
   }
 }
 
+// ---------------------------------------------------------------- read probe
+// Grid-stride streaming read, four 16-byte loads in flight per thread.
+__global__ void __launch_bounds__(NT) amk_read_kernel(const uint4* __restrict__ p, int64_t n16,
+                                                      uint32_t* __restrict__ sink) {
+  const int64_t stride = (int64_t)gridDim.x * NT;
+  int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const uint4 a = ldg<uint4>(p + i), b = ldg<uint4>(p + i + stride);
+    const uint4 c = ldg<uint4>(p + i + 2 * stride), d = ldg<uint4>(p + i + 3 * stride);
+    acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
+  }
+  for (; i < n16; i += stride) {
+    const uint4 a = ldg<uint4>(p + i);
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  sink[(size_t)blockIdx.x * NT + threadIdx.x] = acc;
+}
+
+extern "C" int amk_internal_read_probe(const void* buf, int64_t bytes, int32_t blocks, uint32_t* sink,
+                                       void* stream) {
+  hipLaunchKernelGGL(amk_read_kernel, dim3(blocks), dim3(NT), 0, (hipStream_t)stream, (const uint4*)buf, bytes / 16,
+                     sink);
+  return hipGetLastError() == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
+}
+
 // ---------------------------------------------------------------- host side
 template <int HD, int GM>
 static const void* kernel_ptr(int fmt) {

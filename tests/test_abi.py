@@ -173,3 +173,12 @@ def test_kernels_use_no_scratch(lib):
         fields = dict(x.split("=") for x in kv)
         assert fields["scratch"] == "0" and fields["vgpr_spill"] == "0", (name, fields)
         assert int(fields["vgprs"]) <= 256, (name, fields)
+
+
+def test_read_probe_rejects_bad_arguments(lib):
+    # validated on the host before any device call
+    dummy = ctypes.c_void_p(4096)
+    for nbytes, blocks, buf in ((15, 4, dummy), (0, 4, dummy), (1024, 0, dummy), (1024, 70000, dummy),
+                                (1024, 4, ctypes.c_void_p(4104)), (1024, 4, None)):
+        assert lib.amk_read_probe(buf, nbytes, blocks, dummy, None) == amk.AMK_ERR_INVALID_ARGUMENT
+    assert lib.amk_read_probe(dummy, 1024, 4, None, None) == amk.AMK_ERR_INVALID_ARGUMENT

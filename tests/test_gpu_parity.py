@@ -273,6 +273,27 @@ def test_trace_records(amk, torch_cuda, variant):
     assert set(chained.values()) == {amk.AMK_OP_QKV if variant == "short" else amk.AMK_OP_ATTN}
 
 
+def test_read_probe(amk, torch_cuda):
+    """The streaming-read reference reads every 16-byte vector exactly once:
+    each thread's XOR matches a numpy model of its grid-stride share."""
+    import torch
+    rng = np.random.default_rng(5)
+    words = rng.integers(0, 2**32, size=(1 << 20) // 4 + 4 * 37, dtype=np.uint32)  # a ragged tail of vectors
+    buf = torch.from_numpy(words.view(np.int32)).cuda()
+    blocks = 3
+    sink = torch.zeros(blocks * 512, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    amk.amk_read_probe(buf.data_ptr(), words.nbytes, blocks, sink.data_ptr(), stream.cuda_stream)
+    got = sink.cpu().numpy().view(np.uint32)
+    v = words.reshape(-1, 4)
+    vx = v[:, 0] ^ v[:, 1] ^ v[:, 2] ^ v[:, 3]
+    nthr = blocks * 512
+    want = np.zeros(nthr, dtype=np.uint32)
+    for t in range(nthr):
+        want[t] = np.bitwise_xor.reduce(vx[t::nthr]) if t < len(vx) else 0
+    assert np.array_equal(got, want)
+
+
 def test_invalid_arguments(amk, torch_cuda):
     import torch
     w = weights_for("tiny")
