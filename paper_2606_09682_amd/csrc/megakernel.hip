@@ -421,28 +421,41 @@ __device__ __forceinline__ void consume_block(const uint4 (&buf)[N], int& j, int
 // them after it, since leaving the poll loop depends on the loaded value.
 __device__ __forceinline__ void acquire_after_poll() { __atomic_signal_fence(__ATOMIC_SEQ_CST); }
 
+// How a wait polls.  bf16 weights: two polls in flight (the older one is
+// checked while the newer travels, which halves the time from an increment
+// to its observation), the abort words every 8 spins.  W8A16: one poll and
+// one abort-word load per spin, which measured faster there (its shorter,
+// latency-bound streaming phases suffer from the extra poll traffic).
+template <int FMT> struct Polls { static constexpr bool TWO = FMT == AMK_WEIGHTS_BF16; };
+
+template <int FMT>
 __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t, const amk_task_t* tp, uint32_t epoch,
                                           uint64_t deadline, int lane, uint64_t* tr) {
   const int nw = t.n_wait;
   if (nw == 0) return __hip_atomic_load(m.dev_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
-  uint32_t* p = nullptr;
-  uint32_t target = 0;
-  if (lane < nw) {
-    p = m.counters + ((size_t)ldg<int32_t>(&tp->wait_counter[lane]) * kCounterReplicas +
-                      blockIdx.x % kCounterReplicas) * kCounterStride;
-    target = epoch * (uint32_t)ldg<int32_t>(&tp->wait_count[lane]);
-  }
+  // lanes past n_wait poll the first counter too and never block: the loads
+  // are unconditional, so the compiler counts them exactly
+  const int wl = lane < nw ? lane : 0;
+  const uint32_t* p = m.counters + ((size_t)ldg<int32_t>(&tp->wait_counter[wl]) * kCounterReplicas +
+                                    blockIdx.x % kCounterReplicas) * kCounterStride;
+  const uint32_t target = epoch * (uint32_t)ldg<int32_t>(&tp->wait_count[wl]);
   uint32_t spins = 0;
+  uint32_t v_old = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   for (;;) {
-    bool ok = true;
-    if (lane < nw) ok = (int32_t)(__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) >= 0;
+    uint32_t v_new = 0;
+    if constexpr (Polls<FMT>::TWO) {
+      __builtin_amdgcn_s_sleep(1);
+      v_new = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     const uint64_t now = wall_clock64();
-    if (__all(ok)) break;
-    if (__hip_atomic_load(m.dev_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+    if (__all(lane >= nw || (int32_t)(v_old - target) >= 0)) break;
+    ++spins;
     int code = 0;
+    if (Polls<FMT>::TWO ? (spins & 7u) == 0 : true) {
+      if (__hip_atomic_load(m.dev_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+    }
     // host-mapped flag: read over the bus, so only every 64 spins
-    if ((++spins & 63u) == 0 &&
-        __hip_atomic_load(m.host_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM))
+    if ((spins & 63u) == 0 && __hip_atomic_load(m.host_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM))
       code = AMK_ERR_ABORTED;
     else if (now > deadline)
       code = AMK_ERR_TIMEOUT;
@@ -455,7 +468,12 @@ __device__ __forceinline__ bool wait_deps(const DevModel& m, const amk_task_t& t
       }
       return false;
     }
-    __builtin_amdgcn_s_sleep(1);
+    if constexpr (Polls<FMT>::TWO) {
+      v_old = v_new;
+    } else {
+      __builtin_amdgcn_s_sleep(1);
+      v_old = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_SATISFIED, (uint64_t)wall_clock64());
   acquire_after_poll();
@@ -1189,7 +1207,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     // ---- B1a: the sync wave's counter wait
     if (wave == 0) {
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_WAIT_BEGIN, (uint64_t)wall_clock64());
-      const bool ok = wait_deps(m, t, m.tasks + idx, epoch, deadline, lane, tr);
+      const bool ok = wait_deps<FMT>(m, t, m.tasks + idx, epoch, deadline, lane, tr);
       if (!ok && lane == 0) ctl.abort = 1;
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_WAIT_END, (uint64_t)wall_clock64());
     }
