@@ -1,4 +1,5 @@
-"""CPU oracle of the batch-1 Llama decode step (test infrastructure only).
+"""CPU oracle of the batch-1 Llama decode step, and (schedule_sim) an
+independent safety oracle for its task schedules (test infrastructure only).
 
 Only tests, the smoke check and the benchmark's CPU-baseline leg use this
 package; the product path never imports it.
