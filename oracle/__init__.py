@@ -5,5 +5,5 @@ Only tests, the smoke check and the benchmark's CPU-baseline leg use this
 package; the product path never imports it.
 """
 from .decode import (  # noqa: F401
-    OracleModel, argmax_first, attention, bf16_decode, bf16_round, decode_step, dequantize, greedy,
-    linear, rmsnorm, rope, rope_angles, silu, softmax, top2_margin)
+    OracleModel, argmax_first, attention, bf16_decode, bf16_round, decode_step, dequantize, dequantize_int4,
+    greedy, linear, rmsnorm, rope, rope_angles, silu, softmax, top2_margin, unpack_int4)

@@ -23,8 +23,9 @@ the oracle is the plain definition written out, step by step:
                 h2 = RMSNorm(x, g_mlp);  x = x + Wd (silu(Wg h2) * (Wu h2))
     logits = W_lm RMSNorm(x, g_final);  next = argmax(logits)
 
-W8A16 (paper §5 "Quantized generation": int8 weight-only, dequantisation
-folded into the GEMV) equals the same decode with W' = q * s per row, so the
+W8A16 and W4A16 (paper §5 "Quantized generation": int8 / int4 weight-only,
+dequantisation folded into the GEMV) equal the same decode with W' = q * s
+(s per row for int8, per row and group of input columns for int4), so the
 oracle dequantises explicitly and then runs the plain product.
 
 Readings where the paper is silent (each also listed in the design notes):
@@ -136,6 +137,33 @@ def dequantize(q: np.ndarray, s: np.ndarray, dtype=np.float32) -> np.ndarray:
     return q.astype(dtype) * s.astype(dtype)[:, None]
 
 
+def unpack_int4(packed: np.ndarray) -> np.ndarray:
+    """Signed int4 codes [out, in] of a packed W4A16 matrix [out, in / 2].
+
+    Storage layout: byte i of a row belongs to 32-bit word d = i // 4 at byte
+    position b = i % 4 and holds column 8d + b in its low nibble and column
+    8d + 4 + b in its high nibble, each as the unsigned value code + 8."""
+    p = np.asarray(packed, dtype=np.uint8)
+    rows, nbytes = p.shape
+    codes = np.empty((rows, 2 * nbytes), dtype=np.int16)
+    for i in range(nbytes):
+        d, b = divmod(i, 4)
+        codes[:, 8 * d + b] = (p[:, i] & 0x0F).astype(np.int16) - 8
+        codes[:, 8 * d + 4 + b] = (p[:, i] >> 4).astype(np.int16) - 8
+    return codes
+
+
+def dequantize_int4(packed: np.ndarray, s: np.ndarray, group: int, dtype=np.float32) -> np.ndarray:
+    """W'[r, k] = q[r, k] * s[r, k // group] for int4 weights with one scale
+    per row and group of ``group`` consecutive input columns."""
+    q = unpack_int4(packed).astype(dtype)
+    rows, k = q.shape
+    if s.shape != (rows, k // group) or k % group:
+        raise ValueError("scale shape does not match the packed matrix and group")
+    col_scale = s.astype(dtype)[:, np.arange(k) // group]
+    return q * col_scale
+
+
 def argmax_first(v: np.ndarray) -> int:
     """Index of the maximum, lowest index on ties; NaN is an error."""
     if np.isnan(v).any():
@@ -150,7 +178,7 @@ def argmax_first(v: np.ndarray) -> int:
 class OracleModel:
     """Read-only view of the weights in the oracle's compute precision.
 
-    ``weights`` is a ``synth.Weights``; ``fmt`` is 'bf16' or 'w8a16'.
+    ``weights`` is a ``synth.Weights``; ``fmt`` is 'bf16', 'w8a16' or 'w4a16'.
     Matrices are decoded on demand and optionally cached."""
     weights: object
     fmt: str = "bf16"
@@ -160,7 +188,7 @@ class OracleModel:
     def __post_init__(self):
         self.cfg = self.weights.cfg
         self._cache: Dict[str, np.ndarray] = {}
-        if self.fmt not in ("bf16", "w8a16"):
+        if self.fmt not in ("bf16", "w8a16", "w4a16"):
             raise ValueError(self.fmt)
 
     def vec(self, name: str) -> np.ndarray:
@@ -171,6 +199,8 @@ class OracleModel:
             return self._cache[name]
         if self.fmt == "w8a16" and name in self.weights.q8:
             m = dequantize(self.weights.q8[name], self.weights.scale[name], self.dtype)
+        elif self.fmt == "w4a16" and name in self.weights.q4:
+            m = dequantize_int4(self.weights.q4[name], self.weights.scale4[name], self.weights.group4, self.dtype)
         else:
             m = bf16_decode(self.weights.bf16[name]).astype(self.dtype)
         if self.cache:

@@ -49,6 +49,15 @@ class ModelShape:
             return self.max_seq
         return max(self.positions) + self.greedy_steps + 1
 
+    @property
+    def int4_group(self) -> int:
+        """Default W4A16 group: the largest of 128, 64, 32 that divides every
+        projection's input width (hidden, intermediate, n_heads * head_dim)."""
+        for g in (128, 64, 32):
+            if self.hidden % g == 0 and self.intermediate % g == 0 and self.q_dim % g == 0:
+                return g
+        raise ValueError(f"{self.name}: no int4 group of 32, 64 or 128 divides every input width")
+
     def with_(self, **kw) -> "ModelShape":
         return replace(self, **kw)
 
@@ -59,10 +68,12 @@ class ModelShape:
         return [("wq", self.q_dim, H), ("wk", self.kv_dim, H), ("wv", self.kv_dim, H),
                 ("wo", H, self.q_dim), ("wg", I, H), ("wu", I, H), ("wd", H, I)]
 
-    def algorithmic_bytes(self, fmt: str, pos: int) -> int:
+    def algorithmic_bytes(self, fmt: str, pos: int, group: int = 0) -> int:
         """HBM bytes one decode step must read at least once.
 
-        All GEMV weights (+ fp32 per-row scales for int8), the norm vectors,
+        All GEMV weights (+ fp32 per-row scales for int8, fp16 per-group
+        scales for int4 with ``group`` columns per scale, default
+        ``int4_group``), the norm vectors,
         one gathered embedding row and the K and V rows 0..pos of every layer
         and KV head.  Writes (one K/V row per layer, the logits) are below
         0.01% of this on the large shapes and are not counted."""
@@ -77,6 +88,10 @@ class ModelShape:
         elif fmt == "w8a16":
             lin = lin_elems + 4 * lin_rows
             lm = V * H * 2 if self.tied_embeddings else V * H + 4 * V
+        elif fmt == "w4a16":
+            g = group or self.int4_group
+            lin = lin_elems // 2 + 2 * (lin_elems // g)
+            lm = V * H * 2 if self.tied_embeddings else V * H // 2 + 2 * (V * H // g)
         else:
             raise ValueError(fmt)
         kv_read = L * 2 * self.n_kv_heads * (pos + 1) * self.head_dim * 2

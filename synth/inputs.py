@@ -1,9 +1,9 @@
-"""Seeded synthetic inputs for the decode step: weights, W8A16 weights, KV cache.
+"""Seeded synthetic inputs for the decode step: weights, W8A16 / W4A16 weights, KV cache.
 
 This module is shared by the CPU oracle and the GPU path so that both read
 byte-identical inputs.  It holds no arithmetic of the decode method itself:
 it draws random numbers, rounds them to bf16 storage, and prepares the int8
-weight-only format that the decode step consumes.
+and int4 weight-only formats that the decode step consumes.
 
 Recipe (stands in for the checkpoints the paper uses; the decode latency of a
 batch-1 step depends on shapes and bytes only, paper §5 "Beating cuBLAS with
@@ -18,6 +18,13 @@ int8", which also runs on random-initialised weights at real Llama shapes):
   quantisation): symmetric, one fp32 scale per output row,
   s = max|w| / 127, q = clamp(round_half_even(w / s), -127, 127); an all-zero
   row has s = 0 and q = 0.  The embedding table and a tied LM head stay bf16.
+* W4A16 (paper §5 "Quantized generation": int4 weight-only, round to
+  nearest, fp16 dequantisation scales): symmetric, one fp16 scale per output
+  row and group of ``group`` consecutive input columns,
+  s = fp16(max|w| / 7), q = clamp(round_half_even(w / s), -8, 7) with the
+  division in float32 by the stored (fp16-rounded) scale; an all-zero group
+  has s = 0 and q = 0.  Codes are stored as unsigned nibbles q + 8 in the
+  packed layout of ``pack_int4``.  Same tensors as W8A16 stay bf16.
 
 Every tensor has its own stream: chunk ``c`` of tensor number ``t`` in the
 fixed tensor order is drawn from ``SeedSequence(seed, spawn_key=(t, c))`` with
@@ -96,12 +103,15 @@ def _fill_chunk(seed: int, key: Tuple[int, int], n: int, kind: str, dst: np.ndar
 
 @dataclass
 class Weights:
-    """bf16 weights (uint16 bit patterns) plus optional W8A16 copies."""
+    """bf16 weights (uint16 bit patterns) plus optional W8A16 / W4A16 copies."""
     cfg: ModelShape
     seed: int
     bf16: Dict[str, np.ndarray]
     q8: Dict[str, np.ndarray] = field(default_factory=dict)     # int8 [out, in]
     scale: Dict[str, np.ndarray] = field(default_factory=dict)  # fp32 [out]
+    q4: Dict[str, np.ndarray] = field(default_factory=dict)     # packed int4, uint8 [out, in / 2]
+    scale4: Dict[str, np.ndarray] = field(default_factory=dict) # fp16 [out, in / group4]
+    group4: int = 0                                             # input columns per int4 scale
 
     def lm_head_name(self) -> str:
         return "embed" if self.cfg.tied_embeddings else "lm_head"
@@ -163,6 +173,66 @@ def add_w8a16(w: Weights, threads: Optional[int] = None, row_block: int = 1024) 
     def run(j):
         src, q, s, r0, r1 = j
         q[r0:r1], s[r0:r1] = quantize_rows(src[r0:r1])
+
+    with ThreadPoolExecutor(_threads(threads)) as ex:
+        list(ex.map(run, jobs))
+    return w
+
+
+def pack_int4(q: np.ndarray) -> np.ndarray:
+    """Pack int4 codes q in [-8, 7] of a matrix [out, in] (in a multiple of 8)
+    into bytes [out, in / 2]: the 4 bytes of each 32-bit little-endian word d
+    hold columns 8d .. 8d + 7, byte 4d + b carrying q[8d + b] + 8 in its low
+    nibble and q[8d + 4 + b] + 8 in its high nibble."""
+    q = np.asarray(q)
+    if q.ndim != 2 or q.shape[1] % 8:
+        raise ValueError("need [out, in] with in a multiple of 8")
+    if q.min(initial=0) < -8 or q.max(initial=0) > 7:
+        raise ValueError("int4 codes outside [-8, 7]")
+    u = (q.astype(np.int16) + 8).astype(np.uint8).reshape(q.shape[0], q.shape[1] // 8, 2, 4)
+    return (u[:, :, 0, :] | (u[:, :, 1, :] << np.uint8(4))).reshape(q.shape[0], q.shape[1] // 2)
+
+
+def quantize_groups4(w_bits: np.ndarray, group: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Symmetric round-to-nearest int4 quantisation of a bf16 matrix [out, in]
+    with one fp16 scale per row and ``group`` consecutive input columns.
+
+    Returns (packed uint8 [out, in / 2] in the ``pack_int4`` layout,
+    s float16 [out, in / group]) with s = fp16(max|w| / 7) and
+    q = clamp(round_half_even(w / s), -8, 7) computed in float32 with the
+    stored scale (q = 0 where s == 0)."""
+    w = bf16_bits_to_f32(w_bits).reshape(w_bits.shape)
+    out, k = w.shape
+    if group < 8 or group % 8 or k % group:
+        raise ValueError(f"group {group} must be a multiple of 8 dividing {k}")
+    wg = w.reshape(out, k // group, group)
+    s16 = (np.max(np.abs(wg), axis=2) / np.float32(7.0)).astype(np.float16)
+    if not np.all(np.isfinite(s16)):
+        raise OverflowError("int4 scale outside the fp16 range")
+    s32 = s16.astype(np.float32)
+    safe = np.where(s32 > 0, s32, np.float32(1.0)).astype(np.float32)
+    q = np.clip(np.rint(wg / safe[:, :, None]), -8, 7)
+    q[s32 == 0, :] = 0
+    return pack_int4(q.reshape(out, k).astype(np.int8)), s16
+
+
+def add_w4a16(w: Weights, group: Optional[int] = None, threads: Optional[int] = None,
+              row_block: int = 1024) -> Weights:
+    """Fill ``w.q4`` / ``w.scale4`` / ``w.group4`` for every projection (and an untied LM head)."""
+    g = group if group else w.cfg.int4_group
+    w.group4 = g
+    jobs = []
+    for name in w.quantized_names():
+        src = w.bf16[name]
+        q = np.empty((src.shape[0], src.shape[1] // 2), dtype=np.uint8)
+        s = np.empty((src.shape[0], src.shape[1] // g), dtype=np.float16)
+        w.q4[name], w.scale4[name] = q, s
+        for r0 in range(0, src.shape[0], row_block):
+            jobs.append((src, q, s, r0, min(src.shape[0], r0 + row_block)))
+
+    def run(j):
+        src, q, s, r0, r1 = j
+        q[r0:r1], s[r0:r1] = quantize_groups4(src[r0:r1], g)
 
     with ThreadPoolExecutor(_threads(threads)) as ex:
         list(ex.map(run, jobs))

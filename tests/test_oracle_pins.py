@@ -1,6 +1,8 @@
 """Pins of the CPU oracle against closed forms, brute force, invariants and
 library routines (no GPU).  Each test names what would break it."""
+import json
 import math
+import os
 
 import numpy as np
 import pytest
@@ -219,6 +221,109 @@ def test_dequantized_gemv_within_fp32_bound():
     y64 = (q.astype(np.float64) * s.astype(np.float64)[:, None]) @ x.astype(np.float64)
     bound = 4096 * np.finfo(np.float32).eps * (np.abs(q) * s[:, None]) @ np.abs(x)
     assert np.all(np.abs(y32 - y64) <= bound)
+
+
+# ---------------------------------------------------------------- int4 (W4A16)
+GOLDEN_W4 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "w4a16_layout.json")
+
+
+def test_int4_layout_golden():
+    """Hand-worked example of the packed layout and the group dequantisation
+    (a swapped nibble, a wrong word / byte index, a missing zero point or a
+    wrong group index fails it)."""
+    g = json.load(open(GOLDEN_W4))
+    packed = np.array(g["packed"], dtype=np.uint8)
+    assert oracle.unpack_int4(packed).tolist() == g["codes"]
+    s = np.array(g["scales"], dtype=np.float16)
+    assert oracle.dequantize_int4(packed, s, g["group"]).tolist() == g["dequantized"]
+    # the inputs' packer writes the same bytes for the same codes
+    assert synth.pack_int4(np.array(g["codes"], dtype=np.int8)).tolist() == g["packed"]
+
+
+def test_int4_pack_unpack_are_inverse():
+    # two independent codings of the layout (the inputs' packer, the oracle's unpacker)
+    rng = np.random.default_rng(20)
+    codes = rng.integers(-8, 8, size=(37, 256)).astype(np.int8)
+    assert np.array_equal(oracle.unpack_int4(synth.pack_int4(codes)), codes)
+
+
+@pytest.mark.parametrize("group", [32, 64, 128])
+def test_int4_quantizer_bounds(group):
+    rng = np.random.default_rng(21 + group)
+    w = synth.f32_to_bf16_bits((rng.standard_normal((48, 512)) * 0.02).astype(np.float32))
+    w[5, group:2 * group] = 0  # an all-zero group
+    packed, s = synth.quantize_groups4(w, group)
+    assert packed.shape == (48, 256) and s.shape == (48, 512 // group) and s.dtype == np.float16
+    wf = oracle.bf16_decode(w).astype(np.float64)
+    deq = oracle.dequantize_int4(packed, s, group, np.float64)
+    sc = np.repeat(s.astype(np.float64), group, axis=1)
+    # half a quantisation step, plus one float32 rounding of w / s
+    assert np.all(np.abs(wf - deq) <= sc * 0.5 + np.abs(wf) * 2.0 ** -22)
+    q = oracle.unpack_int4(packed).reshape(48, 512 // group, group)
+    nz = s > 0
+    # s = fp16(max|w| / 7): the largest magnitude of every nonzero group maps to code +-7
+    assert np.all(np.abs(q).max(axis=2)[nz] == 7)
+    assert s[5, 1] == 0 and np.all(q[5, 1] == 0)
+    assert np.all(np.sign(q.reshape(48, 512).astype(np.int32)) * np.sign(wf) >= 0)
+    # the scale is max|w| / 7 rounded to fp16
+    amax = np.abs(wf).reshape(48, 512 // group, group).max(axis=2)
+    assert np.array_equal(s, (amax / 7.0).astype(np.float32).astype(np.float16))
+
+
+def test_int4_quantizer_exact_on_representable_weights():
+    # w = q * 2^-7 with a +-7 in every group: quantisation must return q and s exactly
+    rng = np.random.default_rng(22)
+    q = rng.integers(-7, 8, size=(16, 256))
+    q[:, ::64] = 7 * rng.choice([-1, 1], size=(16, 4))
+    w = synth.f32_to_bf16_bits((q * 2.0 ** -7).astype(np.float32))
+    packed, s = synth.quantize_groups4(w, 64)
+    assert np.all(s == np.float16(2.0 ** -7))
+    assert np.array_equal(oracle.unpack_int4(packed), q)
+    assert np.array_equal(oracle.dequantize_int4(packed, s, 64), oracle.bf16_decode(w).reshape(16, 256))
+
+
+def test_int4_gemv_bruteforce():
+    rng = np.random.default_rng(23)
+    w = synth.f32_to_bf16_bits((rng.standard_normal((6, 96)) * 0.02).astype(np.float32))
+    packed, s = synth.quantize_groups4(w, 32)
+    x = rng.standard_normal(96).astype(np.float32)
+    y = oracle.linear(oracle.dequantize_int4(packed, s, 32), x)
+    for r in range(6):
+        acc = 0.0
+        for k in range(96):
+            byte = int(packed[r, k // 8 * 4 + k % 4])
+            nib = (byte >> 4) if (k % 8) >= 4 else (byte & 15)
+            acc += (nib - 8) * float(s[r, k // 32]) * float(x[k])
+        assert abs(y[r] - acc) <= 96 * 2.0 ** -23 * np.sum(np.abs(oracle.dequantize_int4(packed, s, 32)[r] * x)) + 1e-12
+
+
+W4_TINY = synth.get("tiny").with_(name="tiny_i768", intermediate=768)
+
+
+def test_int4_decode_equals_bf16_decode_on_representable_weights():
+    """Weights that int4 with power-of-two group scales holds exactly: the W4A16
+    decode must equal the bf16 decode bit for bit (wrong matrix, group or
+    LM-head wiring of the int4 path fails it)."""
+    cfg = W4_TINY
+    w = synth.make_weights(cfg, seed=3)
+    rng = np.random.default_rng(24)
+    for name in w.quantized_names():
+        o, k = w.bf16[name].shape
+        q = rng.integers(-7, 8, size=(o, k))
+        q[:, ::64] = 7
+        w.bf16[name] = synth.f32_to_bf16_bits((q * 2.0 ** -9).astype(np.float32))
+    synth.add_w4a16(w, group=64)
+    for name in w.quantized_names():
+        assert np.all(w.scale4[name] == np.float16(2.0 ** -9)), name
+    kv_a = np.zeros(synth.kv_cache_shape(cfg, 4), dtype=np.uint16)
+    kv_b = kv_a.copy()
+    mb = oracle.OracleModel(w, "bf16")
+    m4 = oracle.OracleModel(w, "w4a16")
+    for pos, tok in enumerate((1, 77, 4095)):
+        lb = oracle.decode_step(mb, tok, pos, kv_a)
+        l4 = oracle.decode_step(m4, tok, pos, kv_b)
+        assert np.array_equal(lb, l4)
+    assert np.array_equal(kv_a, kv_b)
 
 
 # ---------------------------------------------------------------- argmax
