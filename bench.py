@@ -3,9 +3,10 @@
 Workload (default): Llama-3-8B-shaped decoder (hidden 4096, 32 layers, 32/8
 heads, head_dim 128, SwiGLU 14336, vocab 128256, untied), seeded random bf16
 weights N(0, 0.02), one decode step of token 1 at position 0.  Variants in
-the same run: W8A16 at position 0 and both formats at position 8192 (KV cache
-filled N(0, 1) bf16).  Every variant is correctness-gated against the CPU
-oracle before its time is reported.
+the same run: W8A16 and W4A16 (int4, fp16 scales per 128 columns) at
+position 0 and all three formats at position 8192 (KV cache filled N(0, 1)
+bf16).  Every variant is correctness-gated against the CPU oracle before its
+time is reported.
 
 A step = one amk_decode_step (one cooperative launch: the whole decode hot
 path).  Inputs are resident in HBM before timing starts; the timed region is
@@ -204,7 +205,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--config", default="llama3_8b")
-    ap.add_argument("--variants", default="all", help="'all' or 'main' (bf16 at position 0 only)")
+    ap.add_argument("--variants", default="all",
+                    help="'all', 'main' (bf16 at position 0 only) or a comma list of FMT@POS, e.g. w4a16@0")
     ap.add_argument("--no-check", action="store_true", help="skip the oracle gate (profiling runs)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
@@ -240,14 +242,20 @@ def main():
     log(f"weights in {time.perf_counter() - t0:.1f}s")
     variants = [("bf16", cfg.positions[0])]
     if args.variants == "all":
-        variants += [("w8a16", cfg.positions[0])] + [(f, cfg.positions[-1]) for f in ("bf16", "w8a16")
-                                                      if cfg.positions[-1] != cfg.positions[0]]
+        variants += [("w8a16", cfg.positions[0]), ("w4a16", cfg.positions[0])] + [
+            (f, cfg.positions[-1]) for f in ("bf16", "w8a16", "w4a16") if cfg.positions[-1] != cfg.positions[0]]
+    elif args.variants != "main":
+        variants = [(v.split("@")[0], int(v.split("@")[1])) for v in args.variants.split(",")]
     results = []
     for fmt, pos in variants:
         if fmt == "w8a16" and not w.q8:
             t0 = time.perf_counter()
             synth.add_w8a16(w)
-            log(f"quantised in {time.perf_counter() - t0:.1f}s")
+            log(f"quantised (int8) in {time.perf_counter() - t0:.1f}s")
+        if fmt == "w4a16" and not w.q4:
+            t0 = time.perf_counter()
+            synth.add_w4a16(w)
+            log(f"quantised (int4, group {w.group4}) in {time.perf_counter() - t0:.1f}s")
         results.append(run_variant(amk, torch, w, fmt, pos, args.steps, args.warmup, check=not args.no_check,
                                    oracle_repeats=3 if not results else 1))
         if results[-1].get("correct") is False or results[-1]["status"] != 0:
@@ -257,7 +265,7 @@ def main():
     peak = None if args.no_check else read_peak_gbs(amk, torch)
     if peak:
         log(f"streaming-read peak {peak:.0f} GB/s")
-    workload = f"{cfg.name}_bf16_pos{cfg.positions[0]}"
+    workload = f"{cfg.name}_{main_res['fmt']}_pos{main_res['pos']}"
     traffic = counter_traffic(workload)
     out = {
         "metric": "µs/token batch-1 decode + achieved HBM GB/s vs weights/BW floor (bf16, W8A16)",
@@ -272,8 +280,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded random weights at the model's shapes, N(0,0.02) bf16)",
-        "config": {"workload": workload, "model_shape": cfg.name, "batch": 1, "position": cfg.positions[0],
-                   "weights": "bf16", "parallelism": "single GPU"},
+        "config": {"workload": workload, "model_shape": cfg.name, "batch": 1, "position": main_res["pos"],
+                   "weights": main_res["fmt"], "parallelism": "single GPU"},
         "correct": ok,
         "roofline": {"bound": "hbm", "achieved": main_res["achieved_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": main_res["achieved_gbs"] / PEAK_HBM_GBS,

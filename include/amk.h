@@ -15,9 +15,11 @@
  * Model family (paper §6 "Architecture coverage"): bias-free projections,
  * full-rotary RoPE (rotate-half pairs i, i + head_dim/2), SiLU-SwiGLU MLP,
  * RMSNorm, grouped-query attention.  Weight formats (paper §5 "Quantized
- * generation"): bf16, or W8A16 = int8 weights with one fp32 scale per output
- * row (symmetric, dequantisation folded into the GEMV).  Activations are fp32
- * throughout; the KV cache is bf16.
+ * generation"; dequantisation folded into the GEMV): bf16; W8A16 = int8
+ * weights with one fp32 scale per output row (symmetric); W4A16 = int4
+ * weights with one fp16 scale per output row and group of group_size input
+ * columns (symmetric, round to nearest; layout under amk_linear_t).
+ * Activations are fp32 throughout; the KV cache is bf16.
  *
  * Conventions for every function:
  *   - returns an int status (AMK_OK or a negative AMK_ERR_*), never throws or
@@ -39,7 +41,7 @@
 extern "C" {
 #endif
 
-#define AMK_ABI_VERSION 3
+#define AMK_ABI_VERSION 4
 
 /* ---- status codes ------------------------------------------------------ */
 enum {
@@ -55,12 +57,13 @@ enum {
   AMK_ERR_ABORTED = -9                /* the host abort flag stopped a launch (sticky) */
 };
 
-enum { AMK_WEIGHTS_BF16 = 0, AMK_WEIGHTS_W8A16 = 1 };
+enum { AMK_WEIGHTS_BF16 = 0, AMK_WEIGHTS_W8A16 = 1, AMK_WEIGHTS_W4A16 = 2 };
 
 /* ---- model description ------------------------------------------------- */
 typedef struct {
   uint32_t abi_version;     /* must be AMK_ABI_VERSION */
-  int32_t hidden;           /* H; H, intermediate and n_heads * head_dim are multiples of 16 */
+  int32_t hidden;           /* H; H, intermediate and n_heads * head_dim are multiples of 16
+                               (of 32 and of group_size under W4A16) */
   int32_t n_layers;         /* L */
   int32_t n_heads;          /* query heads */
   int32_t n_kv_heads;       /* KV heads; n_heads % n_kv_heads == 0, n_heads / n_kv_heads <= 8 */
@@ -71,16 +74,27 @@ typedef struct {
   float rope_theta;
   float rms_eps;
   int32_t tied_embeddings;  /* 1: the LM head is the embedding table (stays bf16) */
-  int32_t weight_format;    /* AMK_WEIGHTS_BF16 or AMK_WEIGHTS_W8A16 */
+  int32_t weight_format;    /* AMK_WEIGHTS_BF16, _W8A16 or _W4A16 */
   int32_t device;           /* HIP device ordinal; -1 = current device */
+  int32_t group_size;       /* W4A16: input columns per scale, a power of two in [32, 1024];
+                               0 = 128.  Ignored by the other formats. */
 } amk_config_t;
 
-/* One projection y = W x.  w: device pointer to a row-major [out, in] matrix
- * (nn.Linear layout), bf16 or int8 per the config; scale: device pointer to
- * fp32[out] for int8 weights, NULL for bf16.  16-byte aligned. */
+/* One projection y = W x, W row-major [out, in] (nn.Linear layout).  w and
+ * scale are device pointers; w is 16-byte aligned.
+ *   bf16:  w = bf16 [out][in]; scale = NULL.
+ *   W8A16: w = int8 [out][in]; scale = fp32 [out] (4-byte aligned);
+ *          W[r][k] = w[r][k] * scale[r].
+ *   W4A16: w = uint8 [out][in / 2]: byte 4d + b of a row (b = 0..3) holds
+ *          column 8d + b in its low nibble and column 8d + 4 + b in its high
+ *          nibble, each nibble the code c in [-8, 7] stored as c + 8;
+ *          scale = fp16 [out][in / group_size] (2-byte aligned);
+ *          W[r][k] = c[r][k] * scale[r][k / group_size].
+ *          (Word d of a row thus carries columns 8d .. 8d + 7, low nibbles
+ *          first: two masks give four byte-sized codes each.) */
 typedef struct {
   const void* w;
-  const float* scale;
+  const void* scale;
 } amk_linear_t;
 
 typedef struct {
@@ -98,7 +112,7 @@ typedef struct {
 typedef struct {
   const void* embed;                 /* bf16 [V, H] device pointer */
   const void* final_norm;            /* bf16 [H] */
-  amk_linear_t lm_head;              /* untied: [V, H] (int8 + scale under W8A16); tied: w = NULL */
+  amk_linear_t lm_head;              /* untied: [V, H] in the weight format; tied: w = NULL */
   const amk_layer_weights_t* layers; /* HOST array [n_layers] of device pointers; read during amk_create only */
 } amk_weights_t;
 

@@ -137,31 +137,33 @@ def dequantize(q: np.ndarray, s: np.ndarray, dtype=np.float32) -> np.ndarray:
     return q.astype(dtype) * s.astype(dtype)[:, None]
 
 
-def unpack_int4(packed: np.ndarray) -> np.ndarray:
-    """Signed int4 codes [out, in] of a packed W4A16 matrix [out, in / 2].
+def unpack_int4(packed: np.ndarray, dtype=np.int16) -> np.ndarray:
+    """Signed int4 codes [out, in] of a packed W4A16 matrix [out, in / 2], as ``dtype``.
 
     Storage layout: byte i of a row belongs to 32-bit word d = i // 4 at byte
     position b = i % 4 and holds column 8d + b in its low nibble and column
     8d + 4 + b in its high nibble, each as the unsigned value code + 8."""
     p = np.asarray(packed, dtype=np.uint8)
     rows, nbytes = p.shape
-    codes = np.empty((rows, 2 * nbytes), dtype=np.int16)
-    for i in range(nbytes):
-        d, b = divmod(i, 4)
-        codes[:, 8 * d + b] = (p[:, i] & 0x0F).astype(np.int16) - 8
-        codes[:, 8 * d + 4 + b] = (p[:, i] >> 4).astype(np.int16) - 8
-    return codes
+    if nbytes % 4:
+        raise ValueError("a packed row is a whole number of 32-bit words")
+    words = p.reshape(rows, nbytes // 4, 4)                    # [row, word d, byte b]
+    codes = np.empty((rows, nbytes // 4, 8), dtype=dtype)     # [row, word d, column 8d + j]
+    codes[:, :, 0:4] = words & 0x0F                            # column 8d + b
+    codes[:, :, 4:8] = words >> 4                              # column 8d + 4 + b
+    codes -= 8
+    return codes.reshape(rows, 2 * nbytes)
 
 
 def dequantize_int4(packed: np.ndarray, s: np.ndarray, group: int, dtype=np.float32) -> np.ndarray:
     """W'[r, k] = q[r, k] * s[r, k // group] for int4 weights with one scale
     per row and group of ``group`` consecutive input columns."""
-    q = unpack_int4(packed).astype(dtype)
+    q = unpack_int4(packed, dtype)
     rows, k = q.shape
     if s.shape != (rows, k // group) or k % group:
         raise ValueError("scale shape does not match the packed matrix and group")
-    col_scale = s.astype(dtype)[:, np.arange(k) // group]
-    return q * col_scale
+    q.reshape(rows, k // group, group)[...] *= s.astype(dtype)[:, :, None]  # column k takes scale k // group
+    return q
 
 
 def argmax_first(v: np.ndarray) -> int:

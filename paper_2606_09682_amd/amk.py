@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libamk.so")
 
 # ---- constants (mirror include/amk.h) ---------------------------------------
-AMK_ABI_VERSION = 3
+AMK_ABI_VERSION = 4
 AMK_OK = 0
 AMK_ERR_INVALID_ARGUMENT = -1
 AMK_ERR_UNSUPPORTED = -2
@@ -28,6 +28,7 @@ AMK_ERR_ABORTED = -9
 
 AMK_WEIGHTS_BF16 = 0
 AMK_WEIGHTS_W8A16 = 1
+AMK_WEIGHTS_W4A16 = 2
 
 AMK_SCHEDULE_SHORT, AMK_SCHEDULE_LONG, AMK_SCHEDULE_TINY = 0, 1, 2
 AMK_TINY_MAX = 8
@@ -49,7 +50,7 @@ class amk_config_t(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("intermediate", ctypes.c_int32), ("vocab", ctypes.c_int32), ("max_seq", ctypes.c_int32),
                 ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float), ("tied_embeddings", ctypes.c_int32),
-                ("weight_format", ctypes.c_int32), ("device", ctypes.c_int32)]
+                ("weight_format", ctypes.c_int32), ("device", ctypes.c_int32), ("group_size", ctypes.c_int32)]
 
 
 class amk_linear_t(ctypes.Structure):
@@ -231,10 +232,10 @@ def amk_schedule_check(cfg: amk_config_t, n_cu: int, tasks, n_counters: int,
 # ---- convenience: a decoder over torch device tensors ---------------------------------
 def make_config(hidden: int, n_layers: int, n_heads: int, n_kv_heads: int, head_dim: int, intermediate: int,
                 vocab: int, max_seq: int, rope_theta: float, rms_eps: float = 1e-5, tied_embeddings: bool = False,
-                weight_format: str = "bf16", device: int = -1) -> amk_config_t:
-    fmt = {"bf16": AMK_WEIGHTS_BF16, "w8a16": AMK_WEIGHTS_W8A16}[weight_format]
+                weight_format: str = "bf16", device: int = -1, group_size: int = 0) -> amk_config_t:
+    fmt = {"bf16": AMK_WEIGHTS_BF16, "w8a16": AMK_WEIGHTS_W8A16, "w4a16": AMK_WEIGHTS_W4A16}[weight_format]
     return amk_config_t(AMK_ABI_VERSION, hidden, n_layers, n_heads, n_kv_heads, head_dim, intermediate, vocab,
-                        max_seq, rope_theta, rms_eps, int(tied_embeddings), fmt, device)
+                        max_seq, rope_theta, rms_eps, int(tied_embeddings), fmt, device, group_size)
 
 
 _PROJ = (("q", "wq"), ("k", "wk"), ("v", "wv"), ("o", "wo"), ("gate", "wg"), ("up", "wu"), ("down", "wd"))
@@ -248,13 +249,17 @@ class Decoder:
     'layers.{l}.attn_norm', 'layers.{l}.mlp_norm' (bf16 [H]) and the
     projections 'layers.{l}.w{q,k,v,o,g,u,d}' [out,in] -- bf16 (any 2-byte
     dtype holding bf16 bits) or, for W8A16, int8 with an fp32 scale tensor
-    under the same name + '.scale'.  The tensors are borrowed: they must
+    under the same name + '.scale', or, for W4A16, packed uint8 [out, in/2]
+    with an fp16 [out, in/group] scale tensor under name + '.scale'.  The
+    tensors are borrowed: they must
     outlive the decoder, which keeps references to them."""
 
     def __init__(self, cfg: amk_config_t, tensors: Mapping[str, "object"], tuning: Optional[amk_tuning_t] = None):
         self.cfg = cfg
         self._keep: Dict[str, object] = dict(tensors)
-        q8 = cfg.weight_format == AMK_WEIGHTS_W8A16
+        quant = cfg.weight_format in (AMK_WEIGHTS_W8A16, AMK_WEIGHTS_W4A16)
+        fmt_name = "W8A16" if cfg.weight_format == AMK_WEIGHTS_W8A16 else "W4A16"
+        scale_size = 4 if cfg.weight_format == AMK_WEIGHTS_W8A16 else 2
 
         def ptr(name):
             t = tensors[name]
@@ -265,7 +270,9 @@ class Decoder:
         def lin(name, quantized):
             if quantized:
                 if tensors[name].element_size() != 1:
-                    raise ValueError(f"{name} must be int8 under W8A16")
+                    raise ValueError(f"{name} must be 1-byte elements under {fmt_name}")
+                if tensors[name + ".scale"].element_size() != scale_size:
+                    raise ValueError(f"{name}.scale must have {scale_size}-byte elements under {fmt_name}")
                 return amk_linear_t(ptr(name), ptr(name + ".scale"))
             if tensors[name].element_size() != 2:
                 raise ValueError(f"{name} must hold bf16 values")
@@ -279,8 +286,8 @@ class Decoder:
             lw.attn_norm = ptr(p + "attn_norm")
             lw.mlp_norm = ptr(p + "mlp_norm")
             for field, name in _PROJ:
-                setattr(lw, field, lin(p + name, q8))
-        lm = amk_linear_t(None, None) if cfg.tied_embeddings else lin("lm_head", q8)
+                setattr(lw, field, lin(p + name, quant))
+        lm = amk_linear_t(None, None) if cfg.tied_embeddings else lin("lm_head", quant)
         self._weights = amk_weights_t(ptr("embed"), ptr("final_norm"), lm, self._layers)
         self.handle = amk_create(cfg, self._weights, tuning)
 

@@ -73,9 +73,10 @@ struct DeviceGuard {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-int check_linear(const amk_linear_t& l, bool int8) {
+int check_linear(const amk_linear_t& l, int fmt) {
   if (!l.w || !aligned16(l.w)) return AMK_ERR_INVALID_ARGUMENT;
-  if (int8 && (!l.scale || ((uintptr_t)l.scale & 3u))) return AMK_ERR_INVALID_ARGUMENT;
+  if (fmt == AMK_WEIGHTS_W8A16 && (!l.scale || ((uintptr_t)l.scale & 3u))) return AMK_ERR_INVALID_ARGUMENT;
+  if (fmt == AMK_WEIGHTS_W4A16 && (!l.scale || ((uintptr_t)l.scale & 1u))) return AMK_ERR_INVALID_ARGUMENT;
   return AMK_OK;
 }
 
@@ -214,12 +215,11 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     if (st != AMK_OK) return st;
 
     // weights: presence, alignment, format
-    const bool q8 = s.fmt == AMK_WEIGHTS_W8A16;
     if (!w->embed || !aligned16(w->embed) || !w->final_norm || !aligned16(w->final_norm) || !w->layers)
       return AMK_ERR_INVALID_ARGUMENT;
     if (s.tied) {
       if (w->lm_head.w) return AMK_ERR_INVALID_ARGUMENT;
-    } else if (check_linear(w->lm_head, q8) != AMK_OK) {
+    } else if (check_linear(w->lm_head, s.fmt) != AMK_OK) {
       return AMK_ERR_INVALID_ARGUMENT;
     }
     for (int l = 0; l < s.L; ++l) {
@@ -228,7 +228,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
         return AMK_ERR_INVALID_ARGUMENT;
       const amk_linear_t* ls[7] = {&lw.q, &lw.k, &lw.v, &lw.o, &lw.gate, &lw.up, &lw.down};
       for (auto* lp : ls)
-        if (check_linear(*lp, q8) != AMK_OK) return AMK_ERR_INVALID_ARGUMENT;
+        if (check_linear(*lp, s.fmt) != AMK_OK) return AMK_ERR_INVALID_ARGUMENT;
     }
 
     h = new amk_handle_s();
@@ -251,14 +251,18 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       return AMK_ERR_SCHEDULE_REJECTED;
     }
 
-    // LDS: activation vector (padded to a whole int8 granule), static
-    // per-row data, residual rows, partials / attention scratch
+    // LDS: activation vector (padded to a whole granule: 1 KiB of weights
+    // covers 1024 int8 or 2048 int4 columns), static per-row data, residual
+    // rows, partials / attention scratch, and under W4A16 the sums of each
+    // 32 consecutive activations
     const int nsw = amk_internal_threads() / 64 - 1;
-    const size_t act = round_up((size_t)std::max({s.H, s.nq * s.hd, s.I}), 1024);
+    const size_t act = round_up((size_t)std::max({s.H, s.nq * s.hd, s.I}), s.fmt == AMK_WEIGHTS_W4A16 ? 2048 : 1024);
+    const size_t act_lds = act + act / 16;  // one float4 of padding per 64 floats (staggered LDS banks)
+    const size_t xsum = s.fmt == AMK_WEIGHTS_W4A16 ? act / 32 : 0;
     // per-wave partial stride in whole float4s keeps every region 16-byte aligned
     const size_t pstride = round_up((size_t)s.max_jobs, 4);
     const size_t scr = std::max<size_t>((size_t)nsw * pstride, (size_t)amk_internal_attn_scratch(s.group, s.hd));
-    const size_t lds_bytes = (act + 3 * pstride + scr) * 4;
+    const size_t lds_bytes = (act_lds + 3 * pstride + scr + xsum) * 4;
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
       free_handle(h);
@@ -342,7 +346,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       const amk_linear_t* ls[7] = {&lw.q, &lw.k, &lw.v, &lw.o, &lw.gate, &lw.up, &lw.down};
       for (int i = 0; i < 7; ++i) {
         layers[l].w[i] = ls[i]->w;
-        layers[l].s[i] = q8 ? ls[i]->scale : nullptr;
+        layers[l].s[i] = s.fmt != AMK_WEIGHTS_BF16 ? ls[i]->scale : nullptr;
       }
       layers[l].attn_norm = (const uint16_t*)lw.attn_norm;
       layers[l].mlp_norm = (const uint16_t*)lw.mlp_norm;
@@ -373,7 +377,9 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     std::memset(&m, 0, sizeof(m));
     m.H = s.H; m.L = L; m.nq = s.nq; m.nkv = s.nkv; m.hd = s.hd; m.I = s.I; m.V = s.V; m.max_seq = s.max_seq;
     m.fmt = s.fmt;
-    m.lm_int8 = q8 && !s.tied;
+    m.lm_fmt = s.tied ? AMK_WEIGHTS_BF16 : s.fmt;
+    m.qglog2 = 0;
+    while (s.qgroup && (1 << m.qglog2) < s.qgroup) ++m.qglog2;
     m.group = s.group; m.half = s.half;
     m.half_log2 = 0;
     while ((1 << m.half_log2) < s.half) ++m.half_log2;
@@ -386,7 +392,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.embed = (const uint16_t*)w->embed;
     m.final_norm = (const uint16_t*)w->final_norm;
     m.lm_w = s.tied ? w->embed : w->lm_head.w;
-    m.lm_s = m.lm_int8 ? w->lm_head.scale : nullptr;
+    m.lm_s = m.lm_fmt != AMK_WEIGHTS_BF16 ? w->lm_head.scale : nullptr;
     m.layers = (const DevLayer*)(base + r_layers.off);
     m.rope = (const float2*)(base + r_rope.off);
     m.x = (float*)(base + r_x.off);
@@ -408,7 +414,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       h->dsch[v].counters = (uint32_t*)(base + r_ctr[v].off);
       h->dsch[v].counter_bytes = r_ctr[v].bytes;
     }
-    m.lds_act = (int32_t)act;
+    m.lds_act = (int32_t)act_lds;
     m.part_stride = (int32_t)pstride;
     m.lds_scr = (int32_t)scr;
     m.lds_bytes = (int32_t)lds_bytes;

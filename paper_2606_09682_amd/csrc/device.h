@@ -12,8 +12,8 @@ namespace amk {
 enum { W_Q = 0, W_K, W_V, W_O, W_G, W_U, W_D, W_COUNT };
 
 struct DevLayer {
-  const void* w[W_COUNT];      // bf16 or int8 [out, in]
-  const float* s[W_COUNT];     // fp32 [out] for int8, else null
+  const void* w[W_COUNT];      // bf16 / int8 [out, in], or packed int4 [out, in / 2]
+  const void* s[W_COUNT];      // fp32 [out] for int8, fp16 [out, in / group] for int4, else null
   const uint16_t* attn_norm;   // bf16 [H]
   const uint16_t* mlp_norm;    // bf16 [H]
 };
@@ -35,7 +35,8 @@ struct DevModel {
   // shape
   int32_t H, L, nq, nkv, hd, I, V, max_seq;
   int32_t fmt;        // AMK_WEIGHTS_*
-  int32_t lm_int8;    // LM head stored as int8 + scales (untied W8A16)
+  int32_t lm_fmt;     // format of the LM head: fmt if untied, AMK_WEIGHTS_BF16 if tied
+  int32_t qglog2;     // W4A16: log2 of the input columns per scale
   int32_t group, half, half_log2, units, q_units, nsplit, n_lm;
   int32_t gq2;        // group + 2: head slots of one KV group in QKV unit order
   int32_t npg;        // QKV tasks per KV group (producers of a group's QKV counter)
@@ -46,7 +47,7 @@ struct DevModel {
   const uint16_t* embed;
   const uint16_t* final_norm;
   const void* lm_w;
-  const float* lm_s;
+  const void* lm_s;
   const DevLayer* layers;    // device array [L]
   // handle-owned tables and scratch
   const float2* rope;        // [max_seq][half] (cos, sin), computed in fp64 on the host
@@ -71,8 +72,9 @@ struct DevModel {
   const amk_task_t* tasks;   // sorted by (cu, seq)
   const int32_t* queue_start;// [n_cu + 1]
   // LDS layout (floats): act[lds_act] stat[2 * part_stride]
-  // res[part_stride] part[lds_scr]
-  int32_t lds_act;           // activation vector region (padded to 1024, zero-filled tail)
+  // res[part_stride] part[lds_scr] xsum[lds_act / 32 under W4A16]
+  int32_t lds_act;           // activation vector region in floats: a whole number of granules'
+                             // elements plus one float4 of padding per 64 floats
   int32_t part_stride;       // rows of one GEMV task at most (partials per streaming wave)
   int32_t lds_scr;           // GEMV partials of all streaming waves, or attention scratch
   int32_t lds_bytes;         // dynamic LDS bytes of one workgroup

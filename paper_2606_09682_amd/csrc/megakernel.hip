@@ -11,7 +11,9 @@
 //               then releases and signals.
 //   waves 1..7  "streaming waves": stream the task's weight rows from HBM in
 //               16-byte-per-lane vectors through a double-buffered register
-//               pipeline and reduce them against the LDS activation.
+//               pipeline and reduce them against the LDS activation (int4
+//               weights: with their fp16 group scales, dequantised in the
+//               dot product).
 //   all waves   load the task's input activation into LDS after the wait (one
 //               round trip), run attention, and run inline continuations.
 //
@@ -56,12 +58,15 @@ namespace amk {
 constexpr int NT = 512;       // threads per workgroup
 constexpr int NW = NT / 64;   // waves
 constexpr int NSW = NW - 1;   // streaming waves
-// Granules per pipeline half, per wave: 4 for bf16 weights, 2 for int8 (an
-// int8 granule holds twice the multiply-adds).  Measured on the Llama-3-8B
-// shape, deeper pipelines delay the sync wave's polls and input loads and
-// stream no faster.
-template <int FMT> struct Pipe { static constexpr int N = FMT == AMK_WEIGHTS_W8A16 ? 2 : 4; };
 constexpr int GRAN = 1024;    // bytes per wave-wide 16-B-per-lane load
+// Granules per pipeline half, per wave: 4 for bf16 weights, 2 for int8 and
+// int4 (their granules hold two and four times the multiply-adds).  Measured
+// on the Llama-3-8B shape, deeper pipelines delay the sync wave's polls and
+// input loads and stream no faster.
+template <int FMT> struct Pipe { static constexpr int N = FMT == AMK_WEIGHTS_BF16 ? 4 : 2; };
+// int4 columns per granule, and per lane (one 16-byte load of 32 nibbles)
+constexpr int GRAN4 = 2 * GRAN;
+constexpr int LANE4 = 32;
 
 struct Ctl {
   int abort;
@@ -228,14 +233,46 @@ __device__ __forceinline__ bool is_normed(int op) {
   return op == AMK_OP_QKV || op == AMK_OP_GATEUP || op == AMK_OP_LMHEAD;
 }
 
+// ---------------------------------------------------------------- LDS regions
+// The task's input activation act[] is padded: element i sits at
+// act_at(i) = i + 4 (i / 64), one unused float4 after every 64 floats.  A
+// lane of a GEMV granule reads 8, 16 or 32 consecutive elements (bf16, int8,
+// int4 weights) with float4 loads, so lanes start 32, 64 or 128 bytes apart
+// and, unpadded, many lanes of one LDS access start in the same bank group
+// (measured on the Llama-3-8B shape: int4 weights decode 1.3x slower
+// unpadded); the padding staggers them.  A lane's elements stay inside one
+// 64-float block, so its loads keep immediate offsets, and a granule's start
+// c * E (E a multiple of 64) moves to c * E * 17 / 16.
+// After act[]:
+//   stat[2 * max_rows]      int8 row scales (rows [0, nj)), then for QKV the
+//                           RoPE (cos, sin) of unit u at [nj + 2u, nj + 2u + 1]
+//   res[max_rows]           residual rows of the last O / down task (or the
+//                           layer-0 embedding rows)
+//   part[...]               per-streaming-wave row partials / attention scratch
+//   xsum[...]               W4A16: xsum[i] = sum of act[32 i .. 32 i + 31]
+__device__ __forceinline__ int act_at(int i) { return i + ((i >> 6) << 2); }
+// act_at(c * E + j) for a granule of E elements (a multiple of 64), j < E
+template <int E>
+__device__ __forceinline__ int act_gran(int c, int j) { return c * (E + E / 16) + act_at(j); }
+
+struct Lds {
+  float* act;
+  float* stat;
+  float* res;
+  float* part;
+  float* xsum;
+};
+
 // ---------------------------------------------------------------- GEMV task geometry
 struct Gemv {
-  int nj;          // rows (jobs)
-  int row_bytes;
-  int gpr;         // granules per row
-  int int8;
-  int tail;        // row_bytes not a multiple of GRAN
-  int G;           // total granules = nj * gpr
+  int nj = 0;          // rows (jobs)
+  int row_bytes = 0;
+  int gpr = 1;         // granules per row
+  int int8 = 0;        // int8 weights, fp32 row scales applied in the epilogue
+  int q4 = 0;          // int4 weights, fp16 group scales applied per granule
+  int tail = 0;        // row_bytes not a multiple of GRAN
+  int G = 0;           // total granules = nj * gpr
+  int srow = 0;        // int4: scale bytes per row
 };
 
 // QKV unit u: head slot u / (d/2) counts KV group by KV group, each group
@@ -269,9 +306,9 @@ __device__ __forceinline__ const uint8_t* mat_base(const DevModel& m, const amk_
   if (mat < 0) return (const uint8_t*)m.lm_w;
   return (const uint8_t*)ldc<const void*>(&m.layers[t.layer].w[mat]);
 }
-__device__ __forceinline__ const float* mat_scale(const DevModel& m, const amk_task_t& t, int mat) {
-  if (mat < 0) return m.lm_s;
-  return ldc<const float*>(&m.layers[t.layer].s[mat]);
+__device__ __forceinline__ const uint8_t* mat_scale(const DevModel& m, const amk_task_t& t, int mat) {
+  if (mat < 0) return (const uint8_t*)m.lm_s;
+  return (const uint8_t*)ldc<const void*>(&m.layers[t.layer].s[mat]);
 }
 
 __device__ __forceinline__ int task_jobs_dev(const amk_task_t& t) {
@@ -290,8 +327,11 @@ __device__ __forceinline__ int task_k(const DevModel& m, const amk_task_t& t) {
 __device__ __forceinline__ Gemv gemv_geom(const DevModel& m, const amk_task_t& t) {
   Gemv g;
   const int K = task_k(m, t);
-  g.int8 = (t.op == AMK_OP_LMHEAD) ? m.lm_int8 : (m.fmt == AMK_WEIGHTS_W8A16);
-  g.row_bytes = g.int8 ? K : 2 * K;
+  const int wf = (t.op == AMK_OP_LMHEAD) ? m.lm_fmt : m.fmt;
+  g.int8 = wf == AMK_WEIGHTS_W8A16;
+  g.q4 = wf == AMK_WEIGHTS_W4A16;
+  g.row_bytes = g.q4 ? K / 2 : g.int8 ? K : 2 * K;
+  g.srow = g.q4 ? (K >> m.qglog2) * 2 : 0;
   g.gpr = (g.row_bytes + GRAN - 1) / GRAN;
   g.tail = (g.row_bytes % GRAN) != 0;
   g.nj = task_jobs_dev(t);
@@ -306,26 +346,31 @@ __device__ __forceinline__ int wave_gbegin(int G, int sw) { return (G * sw) / NS
 struct Cursor {
   int j, c;
   const uint8_t* p;
+  const uint8_t* ps;  // W4A16: the row's fp16 group scales (int4 rows), else p
 };
 
-__device__ __forceinline__ const uint8_t* row_ptr(const DevModel& m, const amk_task_t& t, const Gemv& g, int j) {
+template <int FMT>
+__device__ __forceinline__ void row_ptr(Cursor& cu, const DevModel& m, const amk_task_t& t, const Gemv& g, int j) {
   int mat, row;
   job_row(m, t, j, &mat, &row);
-  return mat_base(m, t, mat) + (size_t)row * g.row_bytes;
+  cu.p = mat_base(m, t, mat) + (size_t)row * g.row_bytes;
+  if constexpr (FMT == AMK_WEIGHTS_W4A16) cu.ps = g.q4 ? mat_scale(m, t, mat) + (size_t)row * g.srow : cu.p;
 }
 
+template <int FMT>
 __device__ __forceinline__ void cursor_init(Cursor& cu, const DevModel& m, const amk_task_t& t, const Gemv& g,
                                             int gidx) {
   cu.j = gidx / g.gpr;
   cu.c = gidx - cu.j * g.gpr;
-  cu.p = row_ptr(m, t, g, cu.j < g.nj ? cu.j : g.nj - 1);
+  row_ptr<FMT>(cu, m, t, g, cu.j < g.nj ? cu.j : g.nj - 1);
 }
 
+template <int FMT>
 __device__ __forceinline__ void cursor_next(Cursor& cu, const DevModel& m, const amk_task_t& t, const Gemv& g) {
   if (++cu.c == g.gpr) {
     cu.c = 0;
     ++cu.j;
-    if (cu.j < g.nj) cu.p = row_ptr(m, t, g, cu.j);
+    if (cu.j < g.nj) row_ptr<FMT>(cu, m, t, g, cu.j);
   }
 }
 
@@ -341,14 +386,24 @@ __device__ __forceinline__ uint4 load_gran(const Cursor& cu, const Gemv& g, int 
   return ldg<uint4>(cu.p + off);
 }
 
-// Issue N granules starting at global granule index gi (clipped to g1).
-template <int N>
-__device__ __forceinline__ void issue_block(uint4 (&buf)[N], Cursor& cu, int& gi, int g1, const DevModel& m,
-                                            const amk_task_t& t, const Gemv& g, int lane) {
+// The fp16 scale of the lane's 32 int4 columns (one group holds whole
+// lanes); tail lanes and rows of other formats re-read a valid address.
+__device__ __forceinline__ uint32_t load_scale4(const Cursor& cu, const DevModel& m, const Gemv& g, int lane) {
+  int idx = (cu.c * GRAN4 + lane * LANE4) >> m.qglog2;
+  if (!g.q4 || (g.tail && cu.c * GRAN + lane * 16 >= g.row_bytes)) idx = 0;
+  return ldg<uint16_t>(cu.ps + 2 * idx);
+}
+
+// Issue N granules starting at global granule index gi (clipped to g1); under
+// W4A16 also each granule's per-lane group scale.
+template <int FMT, int N>
+__device__ __forceinline__ void issue_block(uint4 (&buf)[N], uint32_t (&sc)[N], Cursor& cu, int& gi, int g1,
+                                            const DevModel& m, const amk_task_t& t, const Gemv& g, int lane) {
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     buf[i] = load_gran(cu, g, lane);
-    if (gi < g1) cursor_next(cu, m, t, g);
+    if constexpr (FMT == AMK_WEIGHTS_W4A16) sc[i] = load_scale4(cu, m, g, lane);
+    if (gi < g1) cursor_next<FMT>(cu, m, t, g);
     ++gi;
   }
 }
@@ -356,7 +411,7 @@ __device__ __forceinline__ void issue_block(uint4 (&buf)[N], Cursor& cu, int& gi
 __device__ __forceinline__ float dot_gran(const uint4 v, const float* __restrict__ act, int c, int lane, int int8,
                                           float acc) {
   if (!int8) {
-    const float* x = act + c * (GRAN / 2) + lane * 8;
+    const float* x = act + act_gran<GRAN / 2>(c, lane * 8);
     const float4 a = *reinterpret_cast<const float4*>(x);
     const float4 b = *reinterpret_cast<const float4*>(x + 4);
     acc = fmaf(bf_lo(v.x), a.x, acc); acc = fmaf(bf_hi(v.x), a.y, acc);
@@ -364,7 +419,7 @@ __device__ __forceinline__ float dot_gran(const uint4 v, const float* __restrict
     acc = fmaf(bf_lo(v.z), b.x, acc); acc = fmaf(bf_hi(v.z), b.y, acc);
     acc = fmaf(bf_lo(v.w), b.z, acc); acc = fmaf(bf_hi(v.w), b.w, acc);
   } else {
-    const float* x = act + c * GRAN + lane * 16;
+    const float* x = act + act_gran<GRAN>(c, lane * 16);
     const float4 a = *reinterpret_cast<const float4*>(x);
     const float4 b = *reinterpret_cast<const float4*>(x + 4);
     const float4 d = *reinterpret_cast<const float4*>(x + 8);
@@ -381,17 +436,64 @@ __device__ __forceinline__ float dot_gran(const uint4 v, const float* __restrict
   return acc;
 }
 
+// One int4 granule: the lane's 32 columns [c * 2048 + 32 lane, + 32) of one
+// row, times their group scale s.  Word d of the lane's 16 bytes holds
+// columns 8d .. 8d + 3 in its low nibbles and 8d + 4 .. 8d + 7 in its high
+// nibbles, as unsigned code + 8: masking gives four byte-sized values each,
+// which convert to float one byte at a time (the high ones come out times 16,
+// an exact power of two taken out once).  The zero point leaves
+// sum (code + 8) x - 8 sum x, with sum x over the 32 columns precomputed.
+__device__ __forceinline__ float ub(uint32_t w, int k) { return (float)((w >> (8 * k)) & 0xffu); }
+// w & mask, opaque to the optimiser: with the mask visible it rewrites each
+// byte conversion of the masked word as a bit-field extract plus a
+// conversion, two VALU ops per nibble instead of one v_cvt_f32_ubyteN.
+__device__ __forceinline__ uint32_t low_nibbles(uint32_t w) {
+  uint32_t r;
+  asm("v_and_b32 %0, 0x0f0f0f0f, %1" : "=v"(r) : "v"(w));
+  return r;
+}
+__device__ __forceinline__ uint32_t high_nibbles(uint32_t w) {
+  uint32_t r;
+  asm("v_and_b32 %0, 0xf0f0f0f0, %1" : "=v"(r) : "v"(w));
+  return r;
+}
+__device__ __forceinline__ float dot_gran4(const uint4 v, uint32_t sbits, const float* __restrict__ act,
+                                           const float* __restrict__ xsum, int c, int lane, bool valid, float acc) {
+  const float* x = act + act_gran<GRAN4>(c, lane * LANE4);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  float lo = 0.f, hi = 0.f;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const float4 a = *reinterpret_cast<const float4*>(x + 8 * d);
+    const float4 b = *reinterpret_cast<const float4*>(x + 8 * d + 4);
+    const uint32_t l = low_nibbles(w[d]), h = high_nibbles(w[d]);
+    lo = fmaf(ub(l, 0), a.x, lo); lo = fmaf(ub(l, 1), a.y, lo);
+    lo = fmaf(ub(l, 2), a.z, lo); lo = fmaf(ub(l, 3), a.w, lo);
+    hi = fmaf(ub(h, 0), b.x, hi); hi = fmaf(ub(h, 1), b.y, hi);
+    hi = fmaf(ub(h, 2), b.z, hi); hi = fmaf(ub(h, 3), b.w, hi);
+  }
+  const float u = fmaf(hi, 0.0625f, lo);                       // sum of (code + 8) x
+  const float p = fmaf(-8.f, xsum[c * (GRAN4 / LANE4) + lane], u);  // sum of code x
+  const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)sbits);
+  return valid ? fmaf(s, p, acc) : acc;
+}
+
 // Consume N granules; a finished row's wave-reduced partial goes to part[j].
-template <int N>
-__device__ __forceinline__ void consume_block(const uint4 (&buf)[N], int& j, int& c, int& gi, int g1, float& acc,
-                                              const float* __restrict__ act, float* __restrict__ part,
+template <int FMT, int N>
+__device__ __forceinline__ void consume_block(const uint4 (&buf)[N], const uint32_t (&sc)[N], int& j, int& c, int& gi,
+                                              int g1, float& acc, const Lds& L, float* __restrict__ part,
                                               const Gemv& g, int lane) {
 #pragma unroll
   for (int i = 0; i < N; ++i) {
     if (gi < g1) {
-      uint4 v = buf[i];
-      if (g.tail && c * GRAN + lane * 16 >= g.row_bytes) v = make_uint4(0, 0, 0, 0);
-      acc = dot_gran(v, act, c, lane, g.int8, acc);
+      if (FMT == AMK_WEIGHTS_W4A16 && g.q4) {
+        const bool valid = !g.tail || c * GRAN + lane * 16 < g.row_bytes;
+        acc = dot_gran4(buf[i], sc[i], L.act, L.xsum, c, lane, valid, acc);
+      } else {
+        uint4 v = buf[i];
+        if (g.tail && c * GRAN + lane * 16 >= g.row_bytes) v = make_uint4(0, 0, 0, 0);
+        acc = dot_gran(v, L.act, c, lane, g.int8, acc);
+      }
       if (++c == g.gpr) {
         const float s = wave_sum(acc);
         if (lane == 0) part[j] = s;
@@ -505,18 +607,7 @@ __device__ __forceinline__ bool release_signal_last(const DevModel& m, int count
 // Data of a GEMV task that does not depend on this launch's results and is
 // needed only in its epilogue (int8 row scales, RoPE factors, the layer-0
 // embedding rows of the residual) is fetched by the sync wave while the
-// streaming waves compute.  LDS regions after the activation:
-//   stat[2 * max_rows]      int8 row scales (rows [0, nj)), then for QKV the
-//                           RoPE (cos, sin) of unit u at [nj + 2u, nj + 2u + 1]
-//   res[max_rows]           residual rows of the last O / down task (or the
-//                           layer-0 embedding rows)
-//   part[...]               per-streaming-wave row partials / attention scratch
-struct Lds {
-  float* act;
-  float* stat;
-  float* res;
-  float* part;
-};
+// streaming waves compute.
 
 __device__ __forceinline__ void load_rowdata(const DevModel& m, const amk_task_t& t, int token, int pos,
                                              const Lds& L, Ctl& ctl, int lane) {
@@ -526,7 +617,7 @@ __device__ __forceinline__ void load_rowdata(const DevModel& m, const amk_task_t
     for (int j = lane; j < g.nj; j += 64) {
       int mat, row;
       job_row(m, t, j, &mat, &row);
-      L.stat[j] = ldg<float>(mat_scale(m, t, mat) + row);
+      L.stat[j] = ldg<float>(mat_scale(m, t, mat) + 4 * (size_t)row);
     }
   }
   if (op == AMK_OP_QKV) {
@@ -554,6 +645,9 @@ __device__ __forceinline__ void load_rowdata(const DevModel& m, const amk_task_t
 // Normed inputs load the RMSNorm gain in the same round trip, store x * gain
 // and leave each wave's sum of x^2 in ctl.ssq; the GEMV result is scaled by
 // 1/sqrt(mean(x^2) + eps) in the epilogue (RMSNorm folded into the consumer).
+// Under W4A16 the slices are whole 32-column blocks and each block's sum of
+// the stored values goes to xsum (8 lanes hold one block).
+template <int FMT>
 __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& t, int token, const Lds& L, Ctl& ctl,
                                            int wave, int lane) {
   const int op = t.op;
@@ -576,8 +670,9 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
     default: return;
   }
   const int K = task_k(m, t);
-  const int n4 = K >> 2;  // float4 vectors (K is a multiple of 16)
-  const int v0 = (n4 * wave) / NW, v1 = (n4 * (wave + 1)) / NW;
+  const int n4 = K >> 2;  // float4 vectors (K is a multiple of 16; of 32 under W4A16)
+  constexpr int AL = FMT == AMK_WEIGHTS_W4A16 ? 8 : 1;
+  const int v0 = (n4 / AL * wave) / NW * AL, v1 = (n4 / AL * (wave + 1)) / NW * AL;
   float ss = 0.f;
   constexpr int NB = 8;
   for (int b = v0; b < v1; b += NB * 64) {
@@ -599,13 +694,20 @@ __device__ __forceinline__ void load_input(const DevModel& m, const amk_task_t& 
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int v = b + i * 64 + lane;
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
       if (v < v1) {
-        float4 x = xv[i];
+        x = xv[i];
         if (gain) {
           ss = fmaf(x.x, x.x, ss); ss = fmaf(x.y, x.y, ss); ss = fmaf(x.z, x.z, ss); ss = fmaf(x.w, x.w, ss);
           x = make_float4(x.x * bf_lo(gv[i].x), x.y * bf_hi(gv[i].x), x.z * bf_lo(gv[i].y), x.w * bf_hi(gv[i].y));
         }
-        *reinterpret_cast<float4*>(L.act + v * 4) = x;
+        *reinterpret_cast<float4*>(L.act + act_at(v * 4)) = x;
+      }
+      if constexpr (FMT == AMK_WEIGHTS_W4A16) {
+        // v0 and b are multiples of 8: lanes 8k .. 8k + 7 hold one block,
+        // all in range or all out
+        const float blk = group_sum<8>((x.x + x.y) + (x.z + x.w));
+        if (v < v1 && (lane & 7) == 0) L.xsum[v >> 3] = blk;
       }
     }
   }
@@ -984,9 +1086,10 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
 // takes HR heads per round; lane owns head dims [lane * DPL, (lane + 1) * DPL).
 // All q / K / V loads of a round go out before any arithmetic, once per KV
 // group; positions past pos re-read row pos (clamped, unused).
-template <int HD>
+template <int HD, int FMT>
 __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int pos, const uint16_t* __restrict__ kv,
-                                              float* __restrict__ act, int wave, int lane) {
+                                              float* __restrict__ act, float* __restrict__ xsum, int wave,
+                                              int lane) {
   constexpr int DPL = HD / 64;
   constexpr int HR = 4;
   constexpr int T = AMK_TINY_MAX;
@@ -1058,8 +1161,18 @@ __device__ __forceinline__ void attention_all(const DevModel& m, int layer, int 
       const int h = h0 + i;
       if (h < m.nq) {
         const float inv = 1.0f / l;
+        float blk = 0.f;
 #pragma unroll
-        for (int j = 0; j < DPL; ++j) act[h * HD + lane * DPL + j] = acc[j] * inv;
+        for (int j = 0; j < DPL; ++j) {
+          const float o = acc[j] * inv;
+          act[act_at(h * HD + lane * DPL + j)] = o;
+          blk += o;
+        }
+        if constexpr (FMT == AMK_WEIGHTS_W4A16) {
+          // W4A16 block sums: 32 / DPL lanes hold one 32-column block
+          blk = group_sum<32 / DPL>(blk);
+          if ((lane & (32 / DPL - 1)) == 0) xsum[(h * HD + lane * DPL) >> 5] = blk;
+        }
       }
     }
   }
@@ -1151,6 +1264,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
   L.stat = L.act + m.lds_act;
   L.res = L.stat + 2 * m.part_stride;
   L.part = L.res + m.part_stride;
+  L.xsum = L.part + m.lds_scr;
 
   const int wave = uni(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -1168,6 +1282,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
   // streaming state carried from one task to the next (the weight loads of
   // task idx are issued at the end of task idx - 1)
   uint4 bufA[PIPE], bufB[PIPE];
+  uint32_t scA[PIPE], scB[PIPE];  // W4A16 group scales (unused otherwise)
   Cursor ic;
   int gi = 0, g0 = 0, g1 = 0;
 
@@ -1176,7 +1291,10 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     // redefined on every path, so the buffers are dead between a consumer
     // and the next prefetch (attention and inline tasks reuse the registers)
 #pragma unroll
-    for (int i = 0; i < PIPE; ++i) bufA[i] = bufB[i] = make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < PIPE; ++i) {
+      bufA[i] = bufB[i] = make_uint4(0, 0, 0, 0);
+      scA[i] = scB[i] = 0;
+    }
     if (idx >= qe) return;
     const amk_task_t tn = ldc<amk_task_t>(m.tasks + idx);
     if (!is_gemv(tn.op)) return;
@@ -1186,9 +1304,9 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     g1 = wave_gbegin(gn.G, sw + 1);
     gi = g0;
     if (g0 < g1) {
-      cursor_init(ic, m, tn, gn, g0);
-      issue_block(bufA, ic, gi, g1, m, tn, gn, lane);
-      issue_block(bufB, ic, gi, g1, m, tn, gn, lane);
+      cursor_init<FMT>(ic, m, tn, gn, g0);
+      issue_block<FMT>(bufA, scA, ic, gi, g1, m, tn, gn, lane);
+      issue_block<FMT>(bufB, scB, ic, gi, g1, m, tn, gn, lane);
     }
   };
 
@@ -1200,7 +1318,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
   for (int idx = qb; idx < qe; ++idx) {
     const amk_task_t t = ldc<amk_task_t>(m.tasks + idx);
     const bool gemv = is_gemv(t.op);
-    Gemv g = {0, 0, 1, 0, 0, 0};
+    Gemv g;
     if (gemv) g = gemv_geom(m, t);
     uint64_t* tr = m.trace ? m.trace + (size_t)idx * AMK_TRACE_FIELDS : nullptr;
 
@@ -1222,8 +1340,8 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
 
     // ---- B1b: every wave moves its slice of the input activation
     if (gemv) {
-      if (t.op == AMK_OP_O && t.aux == 1) attention_all<HD>(m, t.layer, pos, kv, L.act, wave, lane);
-      else load_input(m, t, token, L, ctl, wave, lane);
+      if (t.op == AMK_OP_O && t.aux == 1) attention_all<HD, FMT>(m, t.layer, pos, kv, L.act, L.xsum, wave, lane);
+      else load_input<FMT>(m, t, token, L, ctl, wave, lane);
       __syncthreads();
     }
     if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());
@@ -1236,10 +1354,10 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
       int cj = g0 / g.gpr, cc = g0 - cj * g.gpr, cg = g0;
       float acc = 0.f;
       while (cg < g1) {
-        consume_block(bufA, cj, cc, cg, g1, acc, L.act, mypart, g, lane);
-        issue_block(bufA, ic, gi, g1, m, t, g, lane);
-        consume_block(bufB, cj, cc, cg, g1, acc, L.act, mypart, g, lane);
-        issue_block(bufB, ic, gi, g1, m, t, g, lane);
+        consume_block<FMT>(bufA, scA, cj, cc, cg, g1, acc, L, mypart, g, lane);
+        issue_block<FMT>(bufA, scA, ic, gi, g1, m, t, g, lane);
+        consume_block<FMT>(bufB, scB, cj, cc, cg, g1, acc, L, mypart, g, lane);
+        issue_block<FMT>(bufB, scB, ic, gi, g1, m, t, g, lane);
       }
       if (cc != 0) {
         const float s = wave_sum(acc);
@@ -1336,6 +1454,7 @@ extern "C" int amk_internal_read_probe(const void* buf, int64_t bytes, int32_t b
 // ---------------------------------------------------------------- host side
 template <int HD, int GM>
 static const void* kernel_ptr(int fmt) {
+  if (fmt == AMK_WEIGHTS_W4A16) return (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W4A16>;
   return fmt == AMK_WEIGHTS_W8A16 ? (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W8A16>
                                   : (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_BF16>;
 }

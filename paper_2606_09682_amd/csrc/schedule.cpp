@@ -36,7 +36,8 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
     return AMK_ERR_INVALID_ARGUMENT;
   }
   if (L > 65535) { set_msg(why, "n_layers %ld > 65535", L); return AMK_ERR_UNSUPPORTED; }
-  if (cfg->weight_format != AMK_WEIGHTS_BF16 && cfg->weight_format != AMK_WEIGHTS_W8A16) {
+  if (cfg->weight_format != AMK_WEIGHTS_BF16 && cfg->weight_format != AMK_WEIGHTS_W8A16 &&
+      cfg->weight_format != AMK_WEIGHTS_W4A16) {
     set_msg(why, "unknown weight_format %ld", cfg->weight_format);
     return AMK_ERR_INVALID_ARGUMENT;
   }
@@ -59,6 +60,20 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
     set_msg(why, "hidden, intermediate and n_heads*head_dim must be multiples of 16");
     return AMK_ERR_UNSUPPORTED;
   }
+  // W4A16: a 16-byte vector holds 32 columns and one scale covers whole
+  // vectors, so rows are whole vectors and every group a whole number of them
+  int qgroup = 0;
+  if (cfg->weight_format == AMK_WEIGHTS_W4A16) {
+    qgroup = cfg->group_size ? cfg->group_size : 128;
+    if (qgroup < 32 || qgroup > 1024 || (qgroup & (qgroup - 1))) {
+      set_msg(why, "group_size %ld must be a power of two in [32, 1024]", qgroup);
+      return AMK_ERR_INVALID_ARGUMENT;
+    }
+    if (H % qgroup || I % qgroup || (nq * hd) % qgroup) {
+      set_msg(why, "hidden, intermediate and n_heads*head_dim must be multiples of group_size %ld", qgroup);
+      return AMK_ERR_UNSUPPORTED;
+    }
+  }
   int nsplit = tuning && tuning->attn_splits ? tuning->attn_splits : n_cu / nkv;
   nsplit = std::max(1, std::min(nsplit, kMaxAttnSplits));
   if (tuning && tuning->attn_splits && (tuning->attn_splits < 1 || tuning->attn_splits > kMaxAttnSplits)) {
@@ -71,7 +86,7 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
     return AMK_ERR_INVALID_ARGUMENT;
   }
   s->H = H; s->L = L; s->nq = nq; s->nkv = nkv; s->hd = hd; s->I = I; s->V = V; s->max_seq = S;
-  s->fmt = cfg->weight_format; s->tied = cfg->tied_embeddings;
+  s->fmt = cfg->weight_format; s->tied = cfg->tied_embeddings; s->qgroup = qgroup;
   s->group = nq / nkv; s->half = hd / 2;
   s->units = (nq + 2 * nkv) * s->half; s->q_units = nq * s->half;
   s->gunits = (s->group + 2) * s->half;

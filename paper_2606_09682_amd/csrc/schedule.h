@@ -20,6 +20,7 @@ constexpr int kMaxAttnSplits = 64;
 struct Shape {
   int H = 0, L = 0, nq = 0, nkv = 0, hd = 0, I = 0, V = 0, max_seq = 0;
   int fmt = 0, tied = 0;
+  int qgroup = 0;        // W4A16: input columns per scale (0 for the other formats)
   int group = 0;         // query heads per KV head
   int half = 0;          // hd / 2: RoPE row pairs per head
   int units = 0;         // (nq + 2 nkv) * half: q/k/v row-pair units

@@ -49,13 +49,15 @@ def _c_layout():
 int main(void) {
   S(amk_config_t) S(amk_linear_t) S(amk_layer_weights_t) S(amk_weights_t) S(amk_tuning_t) S(amk_task_t)
   S(amk_check_report_t)
-  O(amk_config_t, rope_theta) O(amk_config_t, device) O(amk_layer_weights_t, down) O(amk_weights_t, layers)
+  O(amk_config_t, rope_theta) O(amk_config_t, device) O(amk_config_t, group_size) O(amk_layer_weights_t, down)
+  O(amk_weights_t, layers)
   O(amk_tuning_t, trace) O(amk_tuning_t, short_context) O(amk_tuning_t, tiny_context)
   O(amk_task_t, aux) O(amk_task_t, n_wait) O(amk_task_t, wait_counter) O(amk_task_t, wait_count)
   O(amk_task_t, signal_counter) O(amk_task_t, chain_counter) O(amk_check_report_t, message)
   E(AMK_ABI_VERSION) E(AMK_OK) E(AMK_ERR_INVALID_ARGUMENT) E(AMK_ERR_UNSUPPORTED) E(AMK_ERR_SCHEDULE_REJECTED)
   E(AMK_ERR_OUT_OF_MEMORY) E(AMK_ERR_DEVICE) E(AMK_ERR_COOPERATIVE_UNSUPPORTED) E(AMK_ERR_TIMEOUT)
-  E(AMK_ERR_BAD_STATE) E(AMK_ERR_ABORTED) E(AMK_WEIGHTS_BF16) E(AMK_WEIGHTS_W8A16) E(AMK_MAX_WAITS)
+  E(AMK_ERR_BAD_STATE) E(AMK_ERR_ABORTED) E(AMK_WEIGHTS_BF16) E(AMK_WEIGHTS_W8A16) E(AMK_WEIGHTS_W4A16)
+  E(AMK_MAX_WAITS)
   E(AMK_OP_QKV) E(AMK_OP_ATTN) E(AMK_OP_COMBINE) E(AMK_OP_O) E(AMK_OP_GATEUP) E(AMK_OP_DOWN) E(AMK_OP_LMHEAD)
   E(AMK_OP_ARGMAX) E(AMK_CHECK_OK) E(AMK_CHECK_WELL_FORMED) E(AMK_CHECK_CAPACITY) E(AMK_CHECK_WAIT_SATISFIABLE)
   E(AMK_CHECK_ALL_JOIN) E(AMK_CHECK_ACYCLIC) E(AMK_CHECK_QUEUE_ORDER) E(AMK_CHECK_RACE) E(AMK_CHECK_KV_ORDER)
@@ -120,9 +122,15 @@ def test_kv_cache_bytes(lib, name):
 
 @pytest.mark.parametrize("name", list(synth.CONFIGS))
 @pytest.mark.parametrize("n_cu", [256, 80, 7, 1])
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", ["bf16", "w8a16", "w4a16"])
 def test_every_workload_schedule_is_accepted(lib, name, n_cu, fmt):
-    assert amk.amk_check_config(_cfg(name, fmt), n_cu) == amk.AMK_OK
+    c = synth.get(name)
+    if fmt == "w4a16" and c.intermediate % 32:
+        # int4 rows must be whole 16-byte vectors of 32 columns (tiny: SwiGLU 688)
+        assert amk.amk_check_config(_cfg(name, fmt, group_size=32), n_cu) == amk.AMK_ERR_UNSUPPORTED
+        return
+    over = dict(group_size=c.int4_group) if fmt == "w4a16" else {}
+    assert amk.amk_check_config(_cfg(name, fmt, **over), n_cu) == amk.AMK_OK
 
 
 @pytest.mark.parametrize("over,status", [
@@ -137,6 +145,22 @@ def test_every_workload_schedule_is_accepted(lib, name, n_cu, fmt):
 ])
 def test_unsupported_configs_are_rejected(lib, over, status):
     cfg = _cfg("tiny")
+    for k, v in over.items():
+        setattr(cfg, k, v)
+    assert amk.amk_check_config(cfg, 256) == status
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(group_size=48), amk.AMK_ERR_INVALID_ARGUMENT),    # not a power of two
+    (dict(group_size=16), amk.AMK_ERR_INVALID_ARGUMENT),    # below one lane's 32 columns
+    (dict(group_size=2048), amk.AMK_ERR_INVALID_ARGUMENT),  # above the largest group
+    (dict(group_size=512), amk.AMK_ERR_UNSUPPORTED),        # does not divide hidden 256
+    (dict(intermediate=688, group_size=32), amk.AMK_ERR_UNSUPPORTED),  # 688 not a multiple of 32
+    (dict(group_size=0), amk.AMK_OK),                       # default 128
+    (dict(group_size=256), amk.AMK_OK),
+])
+def test_w4a16_config_rules(lib, over, status):
+    cfg = _cfg("tiny", "w4a16", intermediate=768)
     for k, v in over.items():
         setattr(cfg, k, v)
     assert amk.amk_check_config(cfg, 256) == status
@@ -168,7 +192,7 @@ def test_kernels_use_no_scratch(lib):
     if not os.path.exists(build.RESOURCES):
         build.build()
     rows = [line.split() for line in open(build.RESOURCES) if "amk_decode_kernel" in line]
-    assert len(rows) == 8  # head_dim {64, 128} x group {4, 8} x {bf16, W8A16}
+    assert len(rows) == 12  # head_dim {64, 128} x group {4, 8} x {bf16, W8A16, W4A16}
     for name, *kv in rows:
         fields = dict(x.split("=") for x in kv)
         assert fields["scratch"] == "0" and fields["vgpr_spill"] == "0", (name, fields)

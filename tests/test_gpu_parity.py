@@ -1,8 +1,8 @@
 """GPU decode megakernel vs the CPU oracle on the same seeded inputs.
 
 Bar (per the target): identical greedy tokens and logits within max-abs 2e-2
-of the fp32 oracle for bf16 and W8A16 (W8A16 against the oracle's explicitly
-dequantised weights).  The GPU keeps activations in fp32, so the observed
+of the fp32 oracle for bf16, W8A16 and W4A16 (the quantised formats against
+the oracle's explicitly dequantised weights).  The GPU keeps activations in fp32, so the observed
 error is float reassociation only; the tests also record it.  The appended
 K/V rows must match the oracle's bf16 values to within one bf16 step of the
 larger magnitude plus 1e-5 absolute: both sides round float32 values that
@@ -23,6 +23,7 @@ from synth.device import config_kwargs, kv_from_device, kv_to_device, weights_to
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-2
+FMTS = ["bf16", "w8a16", "w4a16"]
 
 # amk_tuning_t.short_context values forcing one schedule variant
 SHORT_ALWAYS = 1 << 30
@@ -62,23 +63,36 @@ def amk(torch_cuda):
 
 _WEIGHTS = {}
 
+# the tiny decoder with a SwiGLU width int4 groups divide (688 is not a multiple of 32)
+W4_TINY = synth.get("tiny").with_(name="tiny_i768", intermediate=768)
 
-def weights_for(name, seed=0):
-    key = (name, seed)
+
+def weights_for(name, seed=0, fmt="bf16", group=0):
+    """Seeded weights of a named shape (or a ModelShape), with the quantised
+    copies `fmt` needs (int4 with `group` columns per scale, 0 = default)."""
+    cfg = name if isinstance(name, synth.ModelShape) else synth.get(name)
+    key = (cfg, seed)
     if key not in _WEIGHTS:
         _WEIGHTS.clear()
-        cfg = synth.get(name)
-        w = synth.make_weights(cfg, seed=seed)
+        _WEIGHTS[key] = synth.make_weights(cfg, seed=seed)
+    w = _WEIGHTS[key]
+    if fmt == "w8a16" and not w.q8:
         synth.add_w8a16(w)
-        _WEIGHTS[key] = w
-    return _WEIGHTS[key]
+    if fmt == "w4a16" and (not w.q4 or w.group4 != (group or cfg.int4_group)):
+        synth.add_w4a16(w, group=group)
+    return w
+
+
+def tiny_shape(fmt):
+    return W4_TINY if fmt == "w4a16" else synth.get("tiny")
 
 
 def gpu_decode(amk, torch, w, fmt, pos0, steps, kv_np, max_seq, tuning=None):
     cfg = w.cfg
     sc = tuning.short_context if tuning is not None else 0
-    say(f"{cfg.name} {fmt} pos0={pos0} steps={steps} max_seq={max_seq} short_context={sc}")
-    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, fmt, max_seq)), weights_to_device(w, fmt), tuning)
+    group = w.group4 if fmt == "w4a16" else 0
+    say(f"{cfg.name} {fmt} pos0={pos0} steps={steps} max_seq={max_seq} short_context={sc} group={group}")
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, fmt, max_seq, group)), weights_to_device(w, fmt), tuning)
     kv = kv_to_device(kv_np)
     logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
     toks, all_logits = [], []
@@ -129,9 +143,9 @@ def compare(name, fmt, g, o, pos0):
     return err
 
 
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 def test_tiny_greedy(amk, torch_cuda, fmt):
-    w = weights_for("tiny")
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, 0)
     g = gpu_decode(amk, torch_cuda, w, fmt, 0, cfg.greedy_steps, kv, cfg.seq_capacity)
@@ -140,13 +154,13 @@ def test_tiny_greedy(amk, torch_cuda, fmt):
 
 
 @pytest.mark.parametrize("variant", ["short", "long"])
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("pos", [1, 63, 64, 65, 300, 575, 576, 577, 1000])
 def test_tiny_filled_cache(amk, torch_cuda, fmt, pos, variant):
     """Single steps over a cache filled with N(0,1) rows under both schedule
     variants: split boundaries, ragged chunks, and whole-range inline
     attention past one pass of the workgroup (576 rows at head_dim 64)."""
-    w = weights_for("tiny")
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=1024 + 8)
     g = gpu_decode(amk, torch_cuda, w, fmt, pos, 2, kv, kv.shape[3], tuning=tuning_for(amk, variant))
@@ -154,12 +168,12 @@ def test_tiny_filled_cache(amk, torch_cuda, fmt, pos, variant):
     compare(f"tiny {variant}", fmt, g, o, pos)
 
 
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("pos", [0, 1, 6, 7])
 def test_tiny_schedule_positions(amk, torch_cuda, fmt, pos):
     """The tiny schedule (every O task computes all heads' attention itself)
     at the positions it serves, against the oracle and the short schedule."""
-    w = weights_for("tiny")
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=64)
     o = oracle_decode(w, fmt, pos, 1, kv)
@@ -168,10 +182,10 @@ def test_tiny_schedule_positions(amk, torch_cuda, fmt, pos):
         compare(f"tiny {variant}", fmt, g, o, pos)
 
 
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 def test_tiny_attention_split_counts(amk, torch_cuda, fmt):
     """The same step under several attention split counts (1 split .. 64)."""
-    w = weights_for("tiny")
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, 200, seed=1, max_seq=256)
     o = oracle_decode(w, fmt, 200, 1, kv)
@@ -181,10 +195,10 @@ def test_tiny_attention_split_counts(amk, torch_cuda, fmt):
         compare(f"tiny splits={splits}", fmt, g, o, 200)
 
 
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 def test_tiny_small_tasks(amk, torch_cuda, fmt):
     """Row caps of 2 and 6 rows per task: many tiny tasks per queue."""
-    w = weights_for("tiny")
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, 0)
     o = oracle_decode(w, fmt, 0, 3, kv)
@@ -195,9 +209,9 @@ def test_tiny_small_tasks(amk, torch_cuda, fmt):
             compare(f"tiny rows/task={cap} {variant}", fmt, g, o, 0)
 
 
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 def test_smollm2_greedy(amk, torch_cuda, fmt):
-    w = weights_for("smollm2_135m")
+    w = weights_for("smollm2_135m", fmt=fmt)
     cfg = w.cfg
     kv = synth.make_kv_cache(cfg, 0)
     g = gpu_decode(amk, torch_cuda, w, fmt, 0, cfg.greedy_steps, kv, cfg.seq_capacity)
@@ -206,11 +220,11 @@ def test_smollm2_greedy(amk, torch_cuda, fmt):
 
 
 @pytest.mark.parametrize("name", ["tinyllama_1b", "llama32_1b"])
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 def test_1b_positions(amk, torch_cuda, name, fmt):
     """Each position under the variant the step selects by default and under
     the other one."""
-    w = weights_for(name)
+    w = weights_for(name, fmt=fmt)
     cfg = w.cfg
     for pos in cfg.positions:
         kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=pos + 2)
@@ -220,18 +234,33 @@ def test_1b_positions(amk, torch_cuda, name, fmt):
             compare(f"{name} {variant or 'default'}", fmt, g, o, pos)
 
 
-@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+@pytest.mark.parametrize("fmt", FMTS)
 def test_8b_positions(amk, torch_cuda, fmt):
     """Full-size Llama-3-8B shape at positions 0 and 8192 under both schedule
     variants: every logit checked."""
-    w = weights_for("llama3_8b")
+    w = weights_for("llama3_8b", fmt=fmt)
     cfg = w.cfg
-    for pos in cfg.positions:
+    # W4A16: position 0 only (the oracle dequantises every int4 matrix per step);
+    # long contexts of W4A16 run on the 1B shapes
+    for pos in (cfg.positions[:1] if fmt == "w4a16" else cfg.positions):
         kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=pos + 2)
         o = oracle_decode(w, fmt, pos, 1, kv)
         for variant in ("short", "long") + (("tiny",) if pos < amk.AMK_TINY_MAX else ()):
             g = gpu_decode(amk, torch_cuda, w, fmt, pos, 1, kv, kv.shape[3], tuning=tuning_for(amk, variant))
             compare(f"llama3_8b {variant}", fmt, g, o, pos)
+
+
+@pytest.mark.parametrize("group", [32, 64, 256])
+def test_w4a16_group_sizes(amk, torch_cuda, group):
+    """int4 scales over 32 .. 256 columns (one to eight lanes' 32-column blocks
+    per scale) under every schedule variant, a few greedy steps each."""
+    w = weights_for(W4_TINY, fmt="w4a16", group=group)
+    cfg = w.cfg
+    kv = synth.make_kv_cache(cfg, 3, seed=1, max_seq=16)
+    o = oracle_decode(w, "w4a16", 3, 3, kv)
+    for variant in ("tiny", "short", "long"):
+        g = gpu_decode(amk, torch_cuda, w, "w4a16", 3, 3, kv, kv.shape[3], tuning=tuning_for(amk, variant))
+        compare(f"tiny_i768 group={group} {variant}", "w4a16", g, o, 3)
 
 
 @pytest.mark.parametrize("variant", ["short", "long", "tiny"])
