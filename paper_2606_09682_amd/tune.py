@@ -78,7 +78,7 @@ def paired(torch, dec_a, dec_b, step_a, step_b, pairs: int):
 def main(argv: Optional[List[str]] = None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--config", default="llama3_8b")
-    ap.add_argument("--fmt", default="bf16", choices=["bf16", "w8a16"])
+    ap.add_argument("--fmt", default="bf16", choices=["bf16", "w8a16", "w4a16"])
     ap.add_argument("--pos", type=int, default=0)
     ap.add_argument("--pairs", type=int, default=30)
     ap.add_argument("--min-gain", type=float, default=0.005)
@@ -97,6 +97,8 @@ def main(argv: Optional[List[str]] = None) -> int:
     w = synth.make_weights(shape, seed=0)
     if args.fmt == "w8a16":
         synth.add_w8a16(w)
+    elif args.fmt == "w4a16":
+        synth.add_w4a16(w)
     tensors = weights_to_device(w, args.fmt)
     max_seq = args.pos + 2
     cfg = amk.make_config(**config_kwargs(shape, args.fmt, max_seq))
