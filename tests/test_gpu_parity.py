@@ -263,6 +263,18 @@ def test_w4a16_group_sizes(amk, torch_cuda, group):
         compare(f"tiny_i768 group={group} {variant}", "w4a16", g, o, 3)
 
 
+def test_w4a16_largest_group(amk, torch_cuda):
+    """One scale per 1024 input columns (the largest group: 32 lanes' blocks per
+    scale) on the Llama-3.2-1B shape, whose input widths 2048 and 8192 it
+    divides; tied LM head (bf16 inside the int4 kernel)."""
+    w = weights_for("llama32_1b", fmt="w4a16", group=1024)
+    cfg = w.cfg
+    kv = synth.make_kv_cache(cfg, 0, seed=1, max_seq=4)
+    o = oracle_decode(w, "w4a16", 0, 2, kv)
+    g = gpu_decode(amk, torch_cuda, w, "w4a16", 0, 2, kv, kv.shape[3])
+    compare("llama32_1b group=1024", "w4a16", g, o, 0)
+
+
 @pytest.mark.parametrize("variant", ["short", "long", "tiny"])
 def test_trace_records(amk, torch_cuda, variant):
     """Per-task device timestamps are ordered within each task, every task
