@@ -358,17 +358,19 @@ def test_invalid_arguments(amk, torch_cuda):
     dec.close()
 
 
-def test_forced_timeout_is_sticky_and_recoverable(amk, torch_cuda):
+@pytest.mark.parametrize("fmt", FMTS)
+def test_forced_timeout_is_sticky_and_recoverable(amk, torch_cuda, fmt):
     """A 1-microsecond deadline on the kernel's own bounded waits: the launch
     stops every workgroup and reports AMK_ERR_TIMEOUT; later calls return it
-    until reset; a handle with the default deadline still decodes correctly."""
+    until reset; a handle with the default deadline still decodes correctly.
+    Per format, since bf16 and the quantised formats poll in different loops."""
     import torch
-    w = weights_for("tiny")
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
     cfg = w.cfg
     kv_np = synth.make_kv_cache(cfg, 0)
-    say("tiny forced timeout (timeout_us=1)")
-    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", cfg.seq_capacity)), weights_to_device(w, "bf16"),
-                      tuning_for(amk, None, timeout_us=1))
+    say(f"{cfg.name} {fmt} forced timeout (timeout_us=1)")
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, fmt, cfg.seq_capacity, w.group4 if fmt == "w4a16" else 0)),
+                      weights_to_device(w, fmt), tuning_for(amk, None, timeout_us=1))
     kv = kv_to_device(kv_np)
     logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
     dec.step(1, 0, kv, logits)
@@ -380,6 +382,6 @@ def test_forced_timeout_is_sticky_and_recoverable(amk, torch_cuda):
     dec.reset()
     assert dec.status() == amk.AMK_OK
     dec.close()
-    g = gpu_decode(amk, torch_cuda, w, "bf16", 0, 2, kv_np, cfg.seq_capacity)
-    o = oracle_decode(w, "bf16", 0, 2, kv_np)
-    compare("tiny after timeout", "bf16", g, o, 0)
+    g = gpu_decode(amk, torch_cuda, w, fmt, 0, 2, kv_np, cfg.seq_capacity)
+    o = oracle_decode(w, fmt, 0, 2, kv_np)
+    compare(f"{cfg.name} after timeout", fmt, g, o, 0)
