@@ -241,6 +241,48 @@ def make_config(hidden: int, n_layers: int, n_heads: int, n_kv_heads: int, head_
 _PROJ = (("q", "wq"), ("k", "wk"), ("v", "wv"), ("o", "wo"), ("gate", "wg"), ("up", "wu"), ("down", "wd"))
 
 
+def expected_sizes(cfg: amk_config_t) -> Dict[str, int]:
+    """Bytes every weight tensor must have for cfg.  The library receives bare
+    pointers and reads these extents; a smaller tensor would be read past its
+    end on the device, so the binding checks them before amk_create."""
+    H, I, V = cfg.hidden, cfg.intermediate, cfg.vocab
+    qd, kd = cfg.n_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+    shapes = {"wq": (qd, H), "wk": (kd, H), "wv": (kd, H), "wo": (H, qd), "wg": (I, H), "wu": (I, H), "wd": (H, I)}
+    group = cfg.group_size or 128
+
+    def lin(out, inp):
+        if cfg.weight_format == AMK_WEIGHTS_W8A16:
+            return out * inp, 4 * out
+        if cfg.weight_format == AMK_WEIGHTS_W4A16:
+            return out * inp // 2, 2 * out * (inp // group)
+        return 2 * out * inp, 0
+
+    sizes = {"embed": 2 * V * H, "final_norm": 2 * H}
+    names = [(f"layers.{l}.{n}", shapes[n]) for l in range(cfg.n_layers) for n in shapes]
+    if not cfg.tied_embeddings:
+        names.append(("lm_head", (V, H)))
+    for l in range(cfg.n_layers):
+        sizes[f"layers.{l}.attn_norm"] = sizes[f"layers.{l}.mlp_norm"] = 2 * H
+    for name, (out, inp) in names:
+        w, sc = lin(out, inp)
+        sizes[name] = w
+        if sc:
+            sizes[name + ".scale"] = sc
+    return sizes
+
+
+def check_sizes(cfg: amk_config_t, tensors: Mapping[str, "object"]) -> None:
+    """Raise ValueError unless every tensor amk_create will read is present with
+    exactly the bytes cfg implies (device and layout are checked at create)."""
+    for name, nbytes in expected_sizes(cfg).items():
+        if name not in tensors:
+            raise ValueError(f"missing tensor {name}")
+        t = tensors[name]
+        have = t.numel() * t.element_size()
+        if have != nbytes:
+            raise ValueError(f"{name} has {have} bytes, the config needs {nbytes}")
+
+
 class Decoder:
     """One handle over weights that live in torch device tensors.
 
@@ -256,6 +298,7 @@ class Decoder:
 
     def __init__(self, cfg: amk_config_t, tensors: Mapping[str, "object"], tuning: Optional[amk_tuning_t] = None):
         self.cfg = cfg
+        check_sizes(cfg, tensors)
         self._keep: Dict[str, object] = dict(tensors)
         quant = cfg.weight_format in (AMK_WEIGHTS_W8A16, AMK_WEIGHTS_W4A16)
         fmt_name = "W8A16" if cfg.weight_format == AMK_WEIGHTS_W8A16 else "W4A16"
@@ -295,7 +338,13 @@ class Decoder:
         return amk_kv_cache_bytes(self.cfg)
 
     def step(self, token: int, pos: int, kv_cache, logits, stream: Optional[int] = None) -> None:
-        """Enqueue one decode step; kv_cache / logits are device tensors."""
+        """Enqueue one decode step; kv_cache / logits are contiguous device
+        tensors of at least amk_kv_cache_bytes and 4 * vocab bytes."""
+        if not hasattr(self, "_need"):
+            self._need = (amk_kv_cache_bytes(self.cfg), 4 * self.cfg.vocab)
+        for t, need, what in ((kv_cache, self._need[0], "kv_cache"), (logits, self._need[1], "logits")):
+            if not t.is_contiguous() or t.numel() * t.element_size() < need:
+                raise ValueError(f"{what} must be contiguous with at least {need} bytes")
         if stream is None:
             import torch
             stream = torch.cuda.current_stream().cuda_stream

@@ -206,3 +206,33 @@ def test_read_probe_rejects_bad_arguments(lib):
                                 (1024, 4, ctypes.c_void_p(4104)), (1024, 4, None)):
         assert lib.amk_read_probe(buf, nbytes, blocks, dummy, None) == amk.AMK_ERR_INVALID_ARGUMENT
     assert lib.amk_read_probe(dummy, 1024, 4, None, None) == amk.AMK_ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "w8a16", "w4a16"])
+def test_binding_checks_tensor_sizes(fmt):
+    """The binding refuses weight tensors whose byte size differs from what the
+    config implies (the library itself only sees pointers); checked before any
+    device call, so CPU tensors do."""
+    import torch
+    shape = synth.get("tiny").with_(intermediate=768) if fmt == "w4a16" else synth.get("tiny")
+    w = synth.make_weights(shape, seed=0)
+    if fmt == "w8a16":
+        synth.add_w8a16(w)
+    if fmt == "w4a16":
+        synth.add_w4a16(w, group=64)
+    from synth.device import config_kwargs, weights_to_device
+    cfg = amk.make_config(**config_kwargs(shape, fmt, 8, 64 if fmt == "w4a16" else 0))
+    tensors = weights_to_device(w, fmt, device="cpu")
+    amk.check_sizes(cfg, tensors)  # the synthetic tensors fit exactly
+    for victim in ("layers.1.wd", "embed", "layers.0.mlp_norm") + (("layers.2.wk.scale",) if fmt != "bf16" else ()):
+        bad = dict(tensors)
+        bad[victim] = tensors[victim].flatten()[:-1]
+        with pytest.raises(ValueError, match=victim):
+            amk.check_sizes(cfg, bad)
+    bad = dict(tensors)
+    del bad["layers.3.wu"]
+    with pytest.raises(ValueError, match="missing"):
+        amk.check_sizes(cfg, bad)
+    if fmt == "w4a16":  # scales for a different group size have a different extent
+        with pytest.raises(ValueError, match="scale"):
+            amk.check_sizes(amk.make_config(**config_kwargs(shape, fmt, 8, 128)), tensors)
