@@ -973,23 +973,23 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     for (int kb = 0; kb < KB; kb += SB) {
       if (p0 + (kb * NW + wave) * RPW >= n) break;  // no row of this wave from here on
       float sc[GM][SB];
+      // per query head: its LDS values once, then the scores of the SB rows
 #pragma unroll
-      for (int j = 0; j < SB; ++j) {
-        const int k = kb + j;
-        const int r = p0 + (k * NW + wave) * RPW + sub;
-        float kf[EPL];
+      for (int h = 0; h < GM; ++h) {
+        if (h < G) {
+          float q[EPL];
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) kf[e] = row_elem<EPL>(kr[k], e);
+          for (int e = 0; e < EPL; e += 4) {
+            const float4 q4 = *reinterpret_cast<const float4*>(qs + h * HD + c * EPL + e);
+            q[e] = q4.x; q[e + 1] = q4.y; q[e + 2] = q4.z; q[e + 3] = q4.w;
+          }
 #pragma unroll
-        for (int h = 0; h < GM; ++h) {
-          if (h < G) {
+          for (int j = 0; j < SB; ++j) {
+            const int k = kb + j;
+            const int r = p0 + (k * NW + wave) * RPW + sub;
             float d = 0.f;
 #pragma unroll
-            for (int e = 0; e < EPL; e += 4) {
-              const float4 q4 = *reinterpret_cast<const float4*>(qs + h * HD + c * EPL + e);
-              d = fmaf(kf[e], q4.x, d); d = fmaf(kf[e + 1], q4.y, d);
-              d = fmaf(kf[e + 2], q4.z, d); d = fmaf(kf[e + 3], q4.w, d);
-            }
+            for (int e = 0; e < EPL; ++e) d = fmaf(row_elem<EPL>(kr[k], e), q[e], d);
             d = group_sum<LPR>(d) * m.attn_scale;
             sc[h][j] = r < n ? d : -INFINITY;
           }
