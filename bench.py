@@ -212,7 +212,7 @@ def main():
                     help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the decode step is a single-GPU kernel)", file=sys.stderr)
         sys.exit(2)
 
