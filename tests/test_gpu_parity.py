@@ -237,12 +237,10 @@ def test_1b_positions(amk, torch_cuda, name, fmt):
 @pytest.mark.parametrize("fmt", FMTS)
 def test_8b_positions(amk, torch_cuda, fmt):
     """Full-size Llama-3-8B shape at positions 0 and 8192 under both schedule
-    variants: every logit checked."""
+    variants (and the tiny one at 0), every format: every logit checked."""
     w = weights_for("llama3_8b", fmt=fmt)
     cfg = w.cfg
-    # W4A16: position 0 only (the oracle dequantises every int4 matrix per step);
-    # long contexts of W4A16 run on the 1B shapes
-    for pos in (cfg.positions[:1] if fmt == "w4a16" else cfg.positions):
+    for pos in cfg.positions:
         kv = synth.make_kv_cache(cfg, pos, seed=1, max_seq=pos + 2)
         o = oracle_decode(w, fmt, pos, 1, kv)
         for variant in ("short", "long") + (("tiny",) if pos < amk.AMK_TINY_MAX else ()):
