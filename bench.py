@@ -246,6 +246,11 @@ def main():
             (f, cfg.positions[-1]) for f in ("bf16", "w8a16", "w4a16") if cfg.positions[-1] != cfg.positions[0]]
     elif args.variants != "main":
         variants = [(v.split("@")[0], int(v.split("@")[1])) for v in args.variants.split(",")]
+    try:
+        cfg.int4_group
+    except ValueError as e:  # int4 rows need input widths that are multiples of 32
+        log(f"skipping W4A16 variants: {e}")
+        variants = [v for v in variants if v[0] != "w4a16"]
     results = []
     for fmt, pos in variants:
         if fmt == "w8a16" and not w.q8:
