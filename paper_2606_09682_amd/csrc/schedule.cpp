@@ -170,48 +170,63 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
   auto cu_of = [&](int i, int n) { return n >= n_cu ? i % n_cu : (rot + i) % n_cu; };
   auto bump = [&](int n) { if (n < n_cu) rot = (rot + n) % n_cu; };
   auto lo = [](int total, int parts, int i) { return (int)((long)total * i / parts); };
-  // a stage of n tasks over `items` items, all waiting on (wc, wn), signalling sig
-  auto stage = [&](int op, int layer, int items, int jobs_per_item, int wc, int wn) {
+  // A stage's n producers signal kStageCounters counters (task i counter i mod
+  // k), and its consumers wait on each with that counter's producer count:
+  // fewer increments per counter line than one counter for the whole stage.
+  using Waits = std::vector<std::pair<int, int>>;
+  auto stage_counters = [&](int n, int* first) {
+    const int k = std::min(kStageCounters, n);
+    *first = n_ctr;
+    n_ctr += k;
+    Waits w;
+    for (int j = 0; j < k; ++j) w.push_back({*first + j, (n - j + k - 1) / k});
+    return w;
+  };
+  auto sig_of = [&](int first, int n, int i) { return first + i % std::min(kStageCounters, n); };
+  // a stage of n tasks over `items` items, all waiting on `w`; returns its consumers' waits
+  auto stage = [&](int op, int layer, int items, int jobs_per_item, const Waits& w) {
     const int n = n_tasks(items, jobs_per_item);
-    const int sig = n_ctr++;
-    for (int i = 0; i < n; ++i) {
-      std::vector<std::pair<int, int>> w;
-      if (wc >= 0) w.push_back({wc, wn});
-      add(op, layer, cu_of(i, n), lo(items, n, i), lo(items, n, i + 1), 0, w, sig);
-    }
+    int first = 0;
+    const Waits out = stage_counters(n, &first);
+    for (int i = 0; i < n; ++i)
+      add(op, layer, cu_of(i, n), lo(items, n, i), lo(items, n, i + 1), 0, w, sig_of(first, n, i));
     bump(n);
-    return std::make_pair(sig, n);
+    return out;
   };
 
   const bool shortv = variant == AMK_SCHEDULE_SHORT, tinyv = variant == AMK_SCHEDULE_TINY;
-  int prev_c = -1, prev_n = 0;  // counter of the stage producing the layer input
+  Waits prev;  // waits on the stage producing the layer input (none for layer 0)
   for (int l = 0; l < s.L; ++l) {
     // QKV: npg tasks per KV group over that group's units; each group's tasks
-    // signal the group's counter (tiny schedule: one counter for the stage).
-    const int c_qkv0 = n_ctr;
-    n_ctr += tinyv ? 1 : s.nkv;
-    const int c_done = tinyv ? -1 : n_ctr++;  // every KV group's attention output is written
+    // signal the group's counter (tiny schedule: the stage's counters).
     const int n_qkv = s.nkv * s.npg;
+    int c_qkv0 = 0;
+    Waits qkv_out;
+    if (tinyv) {
+      qkv_out = stage_counters(n_qkv, &c_qkv0);
+    } else {
+      c_qkv0 = n_ctr;
+      n_ctr += s.nkv;
+    }
+    const int c_done = tinyv ? -1 : n_ctr++;  // every KV group's attention output is written
     for (int g = 0; g < s.nkv; ++g) {
       for (int i = 0; i < s.npg; ++i) {
-        std::vector<std::pair<int, int>> w;
-        if (prev_c >= 0) w.push_back({prev_c, prev_n});
         const int b = g * s.gunits + lo(s.gunits, s.npg, i), e = g * s.gunits + lo(s.gunits, s.npg, i + 1);
-        add(AMK_OP_QKV, l, cu_of(g * s.npg + i, n_qkv), b, e, g, w, tinyv ? c_qkv0 : c_qkv0 + g,
-            shortv ? c_done : -1);
+        add(AMK_OP_QKV, l, cu_of(g * s.npg + i, n_qkv), b, e, g, prev,
+            tinyv ? sig_of(c_qkv0, n_qkv, g * s.npg + i) : c_qkv0 + g, shortv ? c_done : -1);
       }
     }
     bump(n_qkv);
     if (tinyv) {
       // O tasks compute the attention themselves from q and the KV cache
       const int n = n_tasks(s.H, 1);
-      const int sig = n_ctr++;
+      int first = 0;
+      const Waits o_out = stage_counters(n, &first);
       for (int i = 0; i < n; ++i)
-        add(AMK_OP_O, l, cu_of(i, n), lo(s.H, n, i), lo(s.H, n, i + 1), 1, {{c_qkv0, n_qkv}}, sig);
+        add(AMK_OP_O, l, cu_of(i, n), lo(s.H, n, i), lo(s.H, n, i + 1), 1, qkv_out, sig_of(first, n, i));
       bump(n);
-      auto gu = stage(AMK_OP_GATEUP, l, s.I, 2, sig, n);
-      auto dn = stage(AMK_OP_DOWN, l, s.H, 1, gu.first, gu.second);
-      prev_c = dn.first; prev_n = dn.second;
+      const Waits gu = stage(AMK_OP_GATEUP, l, s.I, 2, o_out);
+      prev = stage(AMK_OP_DOWN, l, s.H, 1, gu);
       continue;
     }
     if (shortv) {
@@ -234,19 +249,19 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
       for (int g = 0; g < s.nkv; ++g)
         add(AMK_OP_COMBINE, l, AMK_CU_INLINE, g * s.group, (g + 1) * s.group, g, {{c_grp0 + g, s.nsplit}}, c_done);
     }
-    auto o = stage(AMK_OP_O, l, s.H, 1, c_done, s.nkv);
-    auto gu = stage(AMK_OP_GATEUP, l, s.I, 2, o.first, o.second);
-    auto dn = stage(AMK_OP_DOWN, l, s.H, 1, gu.first, gu.second);
-    prev_c = dn.first; prev_n = dn.second;
+    const Waits o = stage(AMK_OP_O, l, s.H, 1, {{c_done, s.nkv}});
+    const Waits gu = stage(AMK_OP_GATEUP, l, s.I, 2, o);
+    prev = stage(AMK_OP_DOWN, l, s.H, 1, gu);
   }
   // LM head: one argmax partial slot per task
   {
     const int n = n_tasks(s.V, 1);
-    const int sig = n_ctr++;
+    int first = 0;
+    const Waits lm_out = stage_counters(n, &first);
     for (int i = 0; i < n; ++i)
-      add(AMK_OP_LMHEAD, 0, cu_of(i, n), lo(s.V, n, i), lo(s.V, n, i + 1), i, {{prev_c, prev_n}}, sig);
+      add(AMK_OP_LMHEAD, 0, cu_of(i, n), lo(s.V, n, i), lo(s.V, n, i + 1), i, prev, sig_of(first, n, i));
     bump(n);
-    add(AMK_OP_ARGMAX, 0, cu_of(0, 1), 0, n, 0, {{sig, n}}, -1);
+    add(AMK_OP_ARGMAX, 0, cu_of(0, 1), 0, n, 0, lm_out, -1);
     sch.n_lm_slots = n;
   }
   sch.n_counters = n_ctr;

@@ -15,6 +15,9 @@ namespace amk {
 constexpr int kMaxJobsPerTask = 1024;
 // Largest number of position splits per KV head (one combine lane per split).
 constexpr int kMaxAttnSplits = 64;
+// Counters a wide stage signals (task i counter i mod k); its consumers wait
+// on all of them, so the producers' increments spread over k counter lines.
+constexpr int kStageCounters = 4;
 
 // Derived shape of a validated config.
 struct Shape {

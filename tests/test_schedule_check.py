@@ -167,8 +167,9 @@ def test_kv_read_before_append_rejected(tiny_sched):
 def test_self_wait_rejected(tiny_sched):
     cfg, tasks, nc = tiny_sched
     m = clone(tasks)
-    i = find(m, amk.AMK_OP_GATEUP, 0)
+    i = find(m, amk.AMK_OP_O, 0)  # a task with a free wait slot
     t = m[i]
+    assert t.n_wait < amk.AMK_MAX_WAITS
     c = t.signal_counter
     t.wait_counter[t.n_wait] = c
     t.wait_count[t.n_wait] = len(producers(m, c))
@@ -420,9 +421,15 @@ def test_schedule_shape_8b_tiny(lib):
     assert not [t for t in tasks if t.op in (amk.AMK_OP_ATTN, amk.AMK_OP_COMBINE) or t.cu == amk.AMK_CU_INLINE]
     qkv = [t for t in tasks if t.op == amk.AMK_OP_QKV and t.layer == 7]
     o = [t for t in tasks if t.op == amk.AMK_OP_O and t.layer == 7]
-    assert len({t.signal_counter for t in qkv}) == 1 and all(t.chain_counter == -1 for t in qkv)
-    assert all(t.aux == 1 and t.n_wait == 1 and t.wait_counter[0] == qkv[0].signal_counter and
-               t.wait_count[0] == len(qkv) for t in o)
+    # the QKV stage signals four counters (task i counter i mod 4); every O task
+    # waits on each of them for exactly its producers
+    sigs = {}
+    for t in qkv:
+        sigs[t.signal_counter] = sigs.get(t.signal_counter, 0) + 1
+    assert len(sigs) == 4 and sum(sigs.values()) == len(qkv) and all(t.chain_counter == -1 for t in qkv)
+    for t in o:
+        assert t.aux == 1 and t.n_wait == 4
+        assert {(t.wait_counter[k], t.wait_count[k]) for k in range(t.n_wait)} == set(sigs.items())
 
 
 @pytest.fixture(scope="module")
