@@ -61,9 +61,15 @@ constexpr int NSW = NW - 1;   // streaming waves
 constexpr int GRAN = 1024;    // bytes per wave-wide 16-B-per-lane load
 // Granules per pipeline half, per wave: 4 for bf16 weights, 2 for int8 and
 // int4 (their granules hold two and four times the multiply-adds).  Measured
-// on the Llama-3-8B shape, deeper pipelines delay the sync wave's polls and
-// input loads and stream no faster.
-template <int FMT> struct Pipe { static constexpr int N = FMT == AMK_WEIGHTS_BF16 ? 4 : 2; };
+// on the Llama-3-8B shape, deeper pipelines at a task switch delay the sync
+// wave's polls and input loads and stream no faster.  EXTRA blocks of N
+// granules more are issued once the task's input is in LDS, deepening only
+// the steady state: int8 weights stream faster with two (four blocks in
+// flight); bf16 and int4 weights, bound by VGPRs and by VALU issue, slower.
+template <int FMT> struct Pipe {
+  static constexpr int N = FMT == AMK_WEIGHTS_BF16 ? 4 : 2;
+  static constexpr int EXTRA = FMT == AMK_WEIGHTS_W8A16 ? 2 : 0;
+};
 // int4 columns per granule, and per lane (one 16-byte load of 32 nibbles)
 constexpr int GRAN4 = 2 * GRAN;
 constexpr int LANE4 = 32;
@@ -1252,8 +1258,12 @@ __device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g
 }
 
 // ---------------------------------------------------------------- the kernel
+// Each instantiation starts on a 64 KiB boundary.  The step time of a kernel
+// depends on where its code lies (identical machine code measured 20-50 us
+// apart per 8B step at different offsets), so the alignment keeps every
+// kernel's placement independent of the code size of the others.
 template <int HD, int GM, int FMT>
-__global__ void __launch_bounds__(NT, 1)
+__global__ void __launch_bounds__(NT, 1) __attribute__((aligned(65536)))
 amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16_t* __restrict__ kv,
                   float* __restrict__ logits, uint64_t timeout_ticks) {
   constexpr int PIPE = Pipe<FMT>::N;
@@ -1353,11 +1363,31 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
       float* mypart = L.part + sw * pstride;
       int cj = g0 / g.gpr, cc = g0 - cj * g.gpr, cg = g0;
       float acc = 0.f;
-      while (cg < g1) {
-        consume_block<FMT>(bufA, scA, cj, cc, cg, g1, acc, L, mypart, g, lane);
-        issue_block<FMT>(bufA, scA, ic, gi, g1, m, t, g, lane);
-        consume_block<FMT>(bufB, scB, cj, cc, cg, g1, acc, L, mypart, g, lane);
-        issue_block<FMT>(bufB, scB, ic, gi, g1, m, t, g, lane);
+      constexpr int EX = Pipe<FMT>::EXTRA;
+      if constexpr (EX > 0) {
+        // blocks are consumed in the order they were issued: A, B, X[0], ...
+        uint4 bufX[EX][PIPE];
+        uint32_t scX[EX][PIPE];
+#pragma unroll
+        for (int b = 0; b < EX; ++b) issue_block<FMT>(bufX[b], scX[b], ic, gi, g1, m, t, g, lane);
+        while (cg < g1) {
+          consume_block<FMT>(bufA, scA, cj, cc, cg, g1, acc, L, mypart, g, lane);
+          issue_block<FMT>(bufA, scA, ic, gi, g1, m, t, g, lane);
+          consume_block<FMT>(bufB, scB, cj, cc, cg, g1, acc, L, mypart, g, lane);
+          issue_block<FMT>(bufB, scB, ic, gi, g1, m, t, g, lane);
+#pragma unroll
+          for (int b = 0; b < EX; ++b) {
+            consume_block<FMT>(bufX[b], scX[b], cj, cc, cg, g1, acc, L, mypart, g, lane);
+            issue_block<FMT>(bufX[b], scX[b], ic, gi, g1, m, t, g, lane);
+          }
+        }
+      } else {
+        while (cg < g1) {
+          consume_block<FMT>(bufA, scA, cj, cc, cg, g1, acc, L, mypart, g, lane);
+          issue_block<FMT>(bufA, scA, ic, gi, g1, m, t, g, lane);
+          consume_block<FMT>(bufB, scB, cj, cc, cg, g1, acc, L, mypart, g, lane);
+          issue_block<FMT>(bufB, scB, ic, gi, g1, m, t, g, lane);
+        }
       }
       if (cc != 0) {
         const float s = wave_sum(acc);
