@@ -172,6 +172,18 @@ int amk_schedule_check(const amk_config_t* cfg, const amk_tuning_t* tuning, int3
   }
 }
 
+// Whether the kernel of a schedule runs all its tasks: the tiny-context
+// kernel has no attention tasks, split merges or chained inline tasks, and
+// computes the attention of every O task itself (aux 1); the other kernel
+// computes it in none.
+static bool kernel_runs(const Schedule& sch, bool tiny) {
+  for (const amk_task_t& t : sch.tasks) {
+    if (tiny && (t.op == AMK_OP_ATTN || t.op == AMK_OP_COMBINE || t.chain_counter >= 0)) return false;
+    if (t.op == AMK_OP_O && (t.aux == 1) != tiny) return false;
+  }
+  return true;
+}
+
 int amk_check_config(const amk_config_t* cfg, int32_t n_cu) {
   try {
     Shape s;
@@ -180,7 +192,8 @@ int amk_check_config(const amk_config_t* cfg, int32_t n_cu) {
     for (int v = 0; v < kVariants; ++v) {
       Schedule sch = amk::build_schedule(s, n_cu, v);
       amk_check_report_t rep;
-      if (!amk::check_schedule(s, n_cu, sch.tasks.data(), (int)sch.tasks.size(), sch.n_counters, &rep))
+      if (!amk::check_schedule(s, n_cu, sch.tasks.data(), (int)sch.tasks.size(), sch.n_counters, &rep) ||
+          !kernel_runs(sch, v == AMK_SCHEDULE_TINY))
         return AMK_ERR_SCHEDULE_REJECTED;
     }
     return AMK_OK;
@@ -249,6 +262,14 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
         sl.n_lm_slots != h->sch[AMK_SCHEDULE_TINY].n_lm_slots) {  // the argmax slots are shared
       free_handle(h);
       return AMK_ERR_SCHEDULE_REJECTED;
+    }
+    // each schedule runs on a kernel that carries only its own attention code
+    for (int v = 0; v < kVariants; ++v) {
+      if (!kernel_runs(h->sch[v], v == AMK_SCHEDULE_TINY)) {
+        std::fprintf(stderr, "amk: schedule variant %d has tasks its kernel does not run\n", v);
+        free_handle(h);
+        return AMK_ERR_SCHEDULE_REJECTED;
+      }
     }
 
     // LDS: activation vector (padded to a whole granule: 1 KiB of weights
@@ -450,7 +471,8 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   m.trace = ds.trace;
   m.counters = ds.counters;
   const uint32_t epoch = ds.epoch + 1;  // counter targets are epoch * producers, mod 2^32
-  const int st = amk_internal_launch(&m, token, pos, epoch, (uint16_t*)kv_cache, logits, h->timeout_ticks, stream);
+  const int st = amk_internal_launch(&m, variant == AMK_SCHEDULE_TINY, token, pos, epoch, (uint16_t*)kv_cache, logits,
+                                     h->timeout_ticks, stream);
   if (st != AMK_OK) return st;
   h->last_variant = variant;
   ds.epoch = epoch;

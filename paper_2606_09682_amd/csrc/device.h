@@ -80,8 +80,9 @@ struct DevModel {
   int32_t lds_bytes;         // dynamic LDS bytes of one workgroup
 };
 
-// Launch the decode-step megakernel (defined in megakernel.hip).
-extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos, uint32_t epoch,
+// Launch the decode-step megakernel (defined in megakernel.hip): `tiny` selects
+// the kernel of the tiny-context schedule, which must be the schedule in m.
+extern "C" int amk_internal_launch(const DevModel* m, int32_t tiny, int32_t token, int32_t pos, uint32_t epoch,
                                    uint16_t* kv, float* logits, uint64_t timeout_ticks, void* stream);
 // Threads per workgroup and LDS the kernel needs beyond the model-dependent regions.
 extern "C" int amk_internal_threads(void);

@@ -1258,11 +1258,17 @@ __device__ __forceinline__ void merge_splits(const DevModel& m, int layer, int g
 }
 
 // ---------------------------------------------------------------- the kernel
-// Each instantiation starts on a 64 KiB boundary.  The step time of a kernel
-// depends on where its code lies (identical machine code measured 20-50 us
-// apart per 8B step at different offsets), so the alignment keeps every
-// kernel's placement independent of the code size of the others.
-template <int HD, int GM, int FMT>
+// TINY: the kernel of the tiny-context schedule, whose O tasks compute the
+// attention themselves; the other kernel runs the short and long schedules
+// (attention tasks, the inline attention or split merge of a chain counter).
+// Each carries only its own attention code, so the tiny one stays within
+// 64 KiB of code: the instruction cache then holds it whole, where a larger
+// kernel's lines evict each other depending on where the code lies
+// (identical machine code measured 20-50 us apart per 8B step at different
+// offsets, with instruction-cache misses rising from 6 to 100 thousand per
+// step).  Each instantiation starts on a 64 KiB boundary, so its placement
+// does not depend on the code size of the others.
+template <int HD, int GM, int FMT, bool TINY>
 __global__ void __launch_bounds__(NT, 1) __attribute__((aligned(65536)))
 amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16_t* __restrict__ kv,
                   float* __restrict__ logits, uint64_t timeout_ticks) {
@@ -1350,8 +1356,12 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
 
     // ---- B1b: every wave moves its slice of the input activation
     if (gemv) {
-      if (t.op == AMK_OP_O && t.aux == 1) attention_all<HD, FMT>(m, t.layer, pos, kv, L.act, L.xsum, wave, lane);
-      else load_input<FMT>(m, t, token, L, ctl, wave, lane);
+      if constexpr (TINY) {
+        if (t.op == AMK_OP_O && t.aux == 1) attention_all<HD, FMT>(m, t.layer, pos, kv, L.act, L.xsum, wave, lane);
+        else load_input<FMT>(m, t, token, L, ctl, wave, lane);
+      } else {
+        load_input<FMT>(m, t, token, L, ctl, wave, lane);
+      }
       __syncthreads();
     }
     if (tr && wave == 0 && lane == 0) stg<uint64_t>(tr + AMK_TRACE_INPUT_READY, (uint64_t)wall_clock64());
@@ -1393,14 +1403,16 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         const float s = wave_sum(acc);
         if (lane == 0) mypart[cj] = s;
       }
-    } else if (attn && !idle) {
-      // one split: the normalised output directly; several: a partial record
-      const int j0 = t.begin * chunk, j1 = min(pos + 1, j0 + chunk);
-      const int rec = m.group * (kPartHead + HD);
-      float* dst = active == 1 ? m.o + (size_t)t.layer * m.qs + (size_t)t.aux * m.group * HD
-                               : m.part + (size_t)t.layer * m.ps + ((size_t)t.aux * m.nsplit + t.begin) * rec;
-      attention<HD, GM>(m, t.layer, t.aux, j0, j1, kv, L.act, L.part, dst, active > 1, wave, lane);
-      drain_vmem();
+    } else if constexpr (!TINY) {
+      if (attn && !idle) {
+        // one split: the normalised output directly; several: a partial record
+        const int j0 = t.begin * chunk, j1 = min(pos + 1, j0 + chunk);
+        const int rec = m.group * (kPartHead + HD);
+        float* dst = active == 1 ? m.o + (size_t)t.layer * m.qs + (size_t)t.aux * m.group * HD
+                                 : m.part + (size_t)t.layer * m.ps + ((size_t)t.aux * m.nsplit + t.begin) * rec;
+        attention<HD, GM>(m, t.layer, t.aux, j0, j1, kv, L.act, L.part, dst, active > 1, wave, lane);
+        drain_vmem();
+      }
     }
     __syncthreads();  // B2: GEMV partials in LDS, attention results stored
 
@@ -1431,21 +1443,25 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     }
     __syncthreads();  // B3: results released and signalled
 
-    // ---- inline task of the chain counter (all waves)
-    if (ctl.cont) {
-      if (t.op == AMK_OP_QKV) {
-        float* dst = m.o + (size_t)t.layer * m.qs + (size_t)t.aux * m.group * HD;
-        attention<HD, GM>(m, t.layer, t.aux, 0, pos + 1, kv, L.act, L.part, dst, false, wave, lane);
-      } else if (active > 1) {
-        merge_splits<HD, GM>(m, t.layer, t.aux, active, L.part, wave, lane);
+    // ---- inline task of the chain counter (all waves; never in the tiny schedule)
+    if constexpr (!TINY) {
+      if (ctl.cont) {
+        if (t.op == AMK_OP_QKV) {
+          float* dst = m.o + (size_t)t.layer * m.qs + (size_t)t.aux * m.group * HD;
+          attention<HD, GM>(m, t.layer, t.aux, 0, pos + 1, kv, L.act, L.part, dst, false, wave, lane);
+        } else if (active > 1) {
+          merge_splits<HD, GM>(m, t.layer, t.aux, active, L.part, wave, lane);
+        }
+        drain_vmem();
+        __syncthreads();  // B4: inline results stored
+        if (wave == 0) {
+          release_signal(m, t.chain_counter, lane);
+          if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_CHAINED, (uint64_t)wall_clock64());
+        }
+        __syncthreads();  // B5: the next task's loads go out after the chain signal
+      } else if (tr && wave == 0 && lane == 0) {
+        stg<uint64_t>(tr + AMK_TRACE_CHAINED, 0ull);
       }
-      drain_vmem();
-      __syncthreads();  // B4: inline results stored
-      if (wave == 0) {
-        release_signal(m, t.chain_counter, lane);
-        if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_CHAINED, (uint64_t)wall_clock64());
-      }
-      __syncthreads();  // B5: the next task's loads go out after the chain signal
     } else if (tr && wave == 0 && lane == 0) {
       stg<uint64_t>(tr + AMK_TRACE_CHAINED, 0ull);
     }
@@ -1482,17 +1498,22 @@ extern "C" int amk_internal_read_probe(const void* buf, int64_t bytes, int32_t b
 }
 
 // ---------------------------------------------------------------- host side
-template <int HD, int GM>
+template <int HD, int GM, bool TINY>
 static const void* kernel_ptr(int fmt) {
-  if (fmt == AMK_WEIGHTS_W4A16) return (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W4A16>;
-  return fmt == AMK_WEIGHTS_W8A16 ? (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W8A16>
-                                  : (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_BF16>;
+  if (fmt == AMK_WEIGHTS_W4A16) return (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W4A16, TINY>;
+  return fmt == AMK_WEIGHTS_W8A16 ? (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_W8A16, TINY>
+                                  : (const void*)amk_decode_kernel<HD, GM, AMK_WEIGHTS_BF16, TINY>;
 }
 
-static const void* kernel_for(int head_dim, int group, int fmt) {
+template <int HD, int GM>
+static const void* kernel_ptr(int fmt, bool tiny) {
+  return tiny ? kernel_ptr<HD, GM, true>(fmt) : kernel_ptr<HD, GM, false>(fmt);
+}
+
+static const void* kernel_for(int head_dim, int group, int fmt, bool tiny) {
   const bool small = group <= 4;
-  if (head_dim == 64) return small ? kernel_ptr<64, 4>(fmt) : kernel_ptr<64, 8>(fmt);
-  return small ? kernel_ptr<128, 4>(fmt) : kernel_ptr<128, 8>(fmt);
+  if (head_dim == 64) return small ? kernel_ptr<64, 4>(fmt, tiny) : kernel_ptr<64, 8>(fmt, tiny);
+  return small ? kernel_ptr<128, 4>(fmt, tiny) : kernel_ptr<128, 8>(fmt, tiny);
 }
 
 extern "C" int amk_internal_threads(void) { return NT; }
@@ -1505,24 +1526,36 @@ extern "C" int amk_internal_attn_scratch(int group, int head_dim) {
   return small ? AttnGeom<128, 4>::LDS : AttnGeom<128, 8>::LDS;
 }
 
+// Both kernels of the shape and format (tiny schedule and the others).
 extern "C" int amk_internal_prepare(int head_dim, int group, int fmt, int lds_bytes) {
-  hipError_t e =
-      hipFuncSetAttribute(kernel_for(head_dim, group, fmt), hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
-  return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
+  for (const bool tiny : {true, false}) {
+    const hipError_t e = hipFuncSetAttribute(kernel_for(head_dim, group, fmt, tiny),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+    if (e != hipSuccess) return AMK_ERR_DEVICE;
+  }
+  return AMK_OK;
 }
 
-// Largest number of co-resident workgroups of the kernel per CU for this LDS size.
+// Largest number of co-resident workgroups per CU for this LDS size that
+// both kernels of the shape and format reach.
 extern "C" int amk_internal_occupancy(int head_dim, int group, int fmt, int lds_bytes, int* blocks_per_cu) {
-  hipError_t e =
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, kernel_for(head_dim, group, fmt), NT, lds_bytes);
-  return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
+  int least = 0;
+  for (const bool tiny : {true, false}) {
+    int n = 0;
+    const hipError_t e =
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel_for(head_dim, group, fmt, tiny), NT, lds_bytes);
+    if (e != hipSuccess) return AMK_ERR_DEVICE;
+    least = tiny ? n : (n < least ? n : least);
+  }
+  *blocks_per_cu = least;
+  return AMK_OK;
 }
 
-extern "C" int amk_internal_launch(const DevModel* m, int32_t token, int32_t pos, uint32_t epoch, uint16_t* kv,
-                                   float* logits, uint64_t timeout_ticks, void* stream) {
+extern "C" int amk_internal_launch(const DevModel* m, int32_t tiny, int32_t token, int32_t pos, uint32_t epoch,
+                                   uint16_t* kv, float* logits, uint64_t timeout_ticks, void* stream) {
   DevModel mm = *m;
   void* args[] = {&mm, &token, &pos, &epoch, &kv, &logits, &timeout_ticks};
-  hipError_t e = hipLaunchCooperativeKernel(kernel_for(m->hd, m->group, m->fmt), dim3(m->n_cu), dim3(NT), args,
+  hipError_t e = hipLaunchCooperativeKernel(kernel_for(m->hd, m->group, m->fmt, tiny != 0), dim3(m->n_cu), dim3(NT), args,
                                             (unsigned)m->lds_bytes, (hipStream_t)stream);
   return e == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
 }

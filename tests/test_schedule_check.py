@@ -76,6 +76,15 @@ def test_real_lowering_accepted(lib, name, n_cu, variant):
     assert sorted(seen) == list(range(n_cu))
     for c, seqs in seen.items():
         assert sorted(seqs) == list(range(len(seqs)))
+    # each schedule runs on a kernel that carries only its own attention code:
+    # the tiny one has no attention tasks, merges or chained inline tasks and
+    # computes the attention in every O task (aux 1); the other one in none
+    tiny = variant == amk.AMK_SCHEDULE_TINY
+    for t in tasks:
+        if tiny:
+            assert t.op not in (amk.AMK_OP_ATTN, amk.AMK_OP_COMBINE) and t.chain_counter == -1
+        if t.op == amk.AMK_OP_O:
+            assert t.aux == (1 if tiny else 0)
 
 
 def test_schedule_shape_8b(lib):
