@@ -884,7 +884,7 @@ struct AttnGeom {
   static constexpr int LPR = HD / EPL;
   static constexpr int RPW = 64 / LPR;
   static constexpr int KB = 9;
-  static constexpr int SB = 3;  // rows per lane per softmax update
+  static constexpr int SB = 3;  // most rows per lane per softmax update
   static constexpr int RP = NW * RPW * KB;
   // LDS scratch (floats): per-wave accumulators red[NW][GM][HD] and running
   // (max, sum) stat[NW][GM][2]; the split merge reuses the region
@@ -918,6 +918,9 @@ __device__ __forceinline__ float row_elem(const RowVec<EPL>& r, int e) {
 // flash-decoding family this follows).  Every wave keeps its own running
 // max / sum / accumulators over the rows it loads (online softmax, no
 // barrier inside the position loop); the waves merge through LDS at the end.
+// The queries are stored pre-multiplied by log2(e) / sqrt(d), so scores and
+// maxima are in log2 units and each softmax weight is one exp2: the same
+// weights as exp(q.k / sqrt(d) - max), up to fp32 rounding.
 // `record`: store per head (m, l, unnormalised acc) at dst[h * (kPartHead +
 // d)], else the normalised output at dst[h * d].  Stores are issued by every
 // wave; the caller drains them.
@@ -928,7 +931,7 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
                                           int lane) {
   using A = AttnGeom<HD, GM>;
   constexpr int EPL = A::EPL, LPR = A::LPR, RPW = A::RPW, KB = A::KB, SB = A::SB, RP = A::RP;
-  static_assert(KB % SB == 0, "sub-batches");
+  static_assert(KB == 9 && SB == 3, "sub-batches of 3, 3, 2 and 1 row slots");
   const int G = m.group;
   const int n = j1 - j0;
   const int sub = lane / LPR, c = lane % LPR;
@@ -951,7 +954,10 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
   static_assert(GM * HD / 4 <= NT, "one query vector per thread");
   if ((int)threadIdx.x < G * HD / 4) {
     const float* qsrc = m.q + (size_t)layer * m.qs + (size_t)g * G * HD;
-    *reinterpret_cast<float4*>(qs + 4 * threadIdx.x) = ldg<float4>(qsrc + 4 * threadIdx.x);
+    const float c = m.attn_scale * 1.4426950408889634f;  // log2(e) / sqrt(d)
+    float4 qv = ldg<float4>(qsrc + 4 * threadIdx.x);
+    qv.x *= c; qv.y *= c; qv.z *= c; qv.w *= c;
+    *reinterpret_cast<float4*>(qs + 4 * threadIdx.x) = qv;
   }
   for (int p0 = 0; p0 < n; p0 += RP) {
     // rows of this lane: r_k = p0 + (k * NW + wave) * RPW + sub.  Every load
@@ -971,12 +977,16 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
       }
     }
     if (p0 == 0) __syncthreads();
-    // rows in sub-batches of SB: scores for every query head, then one
-    // online-softmax update per head and sub-batch.  The running max / sum
+    // rows in sub-batches of 3, 3, 2 and 1 slots: scores for every query
+    // head, then one online-softmax update per head and sub-batch.  A wave
+    // whose range ends after 8 slots skips the last one instead of scoring a
+    // fully masked slot.  The running max / sum
     // belong to the lane's row group (LPR lanes sharing its rows), so no
     // cross-lane maximum is needed inside the loop.
 #pragma unroll
-    for (int kb = 0; kb < KB; kb += SB) {
+    for (int sb = 0; sb < 4; ++sb) {
+      const int kb = sb == 0 ? 0 : sb == 1 ? 3 : sb == 2 ? 6 : 8;
+      const int NB = sb < 2 ? 3 : sb == 2 ? 2 : 1;
       if (p0 + (kb * NW + wave) * RPW >= n) break;  // no row of this wave from here on
       float sc[GM][SB];
       // per query head: its LDS values once, then the scores of the SB rows
@@ -990,13 +1000,13 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
             q[e] = q4.x; q[e + 1] = q4.y; q[e + 2] = q4.z; q[e + 3] = q4.w;
           }
 #pragma unroll
-          for (int j = 0; j < SB; ++j) {
+          for (int j = 0; j < NB; ++j) {
             const int k = kb + j;
             const int r = p0 + (k * NW + wave) * RPW + sub;
             float d = 0.f;
 #pragma unroll
             for (int e = 0; e < EPL; ++e) d = fmaf(row_elem<EPL>(kr[k], e), q[e], d);
-            d = group_sum<LPR>(d) * m.attn_scale;
+            d = group_sum<LPR>(d);
             sc[h][j] = r < n ? d : -INFINITY;
           }
         }
@@ -1006,15 +1016,15 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
         if (h < G) {
           float mx = sc[h][0];
 #pragma unroll
-          for (int j = 1; j < SB; ++j) mx = fmaxf(mx, sc[h][j]);
+          for (int j = 1; j < NB; ++j) mx = fmaxf(mx, sc[h][j]);
           const float m_new = fmaxf(m_run[h], mx);
           // a row group that has seen no row keeps (-inf, 0, 0)
           const float mref = m_new == -INFINITY ? 0.f : m_new;
-          const float alpha = __expf(m_run[h] - mref);
+          const float alpha = __builtin_amdgcn_exp2f(m_run[h] - mref);
           float ls = 0.f;
 #pragma unroll
-          for (int j = 0; j < SB; ++j) {
-            sc[h][j] = __expf(sc[h][j] - mref);
+          for (int j = 0; j < NB; ++j) {
+            sc[h][j] = __builtin_amdgcn_exp2f(sc[h][j] - mref);
             ls += sc[h][j];
           }
           l_run[h] = l_run[h] * alpha + ls;
@@ -1024,7 +1034,7 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
         }
       }
 #pragma unroll
-      for (int j = 0; j < SB; ++j) {
+      for (int j = 0; j < NB; ++j) {
         float vf[EPL];
 #pragma unroll
         for (int e = 0; e < EPL; ++e) vf[e] = row_elem<EPL>(vr[kb + j], e);
@@ -1047,7 +1057,7 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     if (h < G) {
       // merge the row groups of the wave: rescale each to the wave's max
       const float M = across_max<LPR>(m_run[h]);
-      const float f = m_run[h] == -INFINITY ? 0.f : __expf(m_run[h] - M);
+      const float f = m_run[h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[h] - M);
       const float l = across_sum<LPR>(l_run[h] * f);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
@@ -1071,7 +1081,7 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     for (int w = 0; w < NW; ++w) {
       const float mw = stat[(w * GM + h) * 2];
       if (mw != -INFINITY) {
-        const float f = __expf(mw - M);
+        const float f = __builtin_amdgcn_exp2f(mw - M);
         l = fmaf(f, stat[(w * GM + h) * 2 + 1], l);
         o = fmaf(f, red[(w * GM + h) * HD + d], o);
       }
@@ -1079,7 +1089,8 @@ __device__ __forceinline__ void attention(const DevModel& m, int layer, int g, i
     if (record) {
       float* rec = dst + h * (kPartHead + HD);
       stc(rec + kPartHead + d, o);
-      if (d == 0) stc(reinterpret_cast<float2*>(rec), make_float2(M, l));
+      // the record's maximum in natural-log units, as the split merge reads it
+      if (d == 0) stc(reinterpret_cast<float2*>(rec), make_float2(M * 0.6931471805599453f, l));
     } else {
       stc(dst + h * HD + d, o / l);
     }
