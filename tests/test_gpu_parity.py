@@ -196,6 +196,22 @@ def test_tiny_attention_split_counts(amk, torch_cuda, fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
+def test_tiny_attention_sub_batches(amk, torch_cuda, fmt):
+    """Split lengths that reach every softmax sub-batch of a pass (row slots
+    3, 3, 2, 1) and a second pass: at pos 1000 one split holds 1001 rows (a
+    full pass of 576, then 425), two splits 501 rows each (the last wave's
+    eighth slot masked)."""
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
+    cfg = w.cfg
+    kv = synth.make_kv_cache(cfg, 1000, seed=1, max_seq=1024 + 8)
+    o = oracle_decode(w, fmt, 1000, 1, kv)
+    for splits in (1, 2):
+        t = tuning_for(amk, "long", attn_splits=splits)
+        g = gpu_decode(amk, torch_cuda, w, fmt, 1000, 1, kv, kv.shape[3], tuning=t)
+        compare(f"tiny splits={splits} pos 1000", fmt, g, o, 1000)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
 def test_tiny_small_tasks(amk, torch_cuda, fmt):
     """Row caps of 2 and 6 rows per task: many tiny tasks per queue."""
     w = weights_for(tiny_shape(fmt), fmt=fmt)
