@@ -23,8 +23,18 @@ A schedule is unsafe if any label says so.  Like the paper's counter-driven
 oracle, the dynamic part only observes races that some sampled interleaving
 exhibits (a wait count below the producer count, for instance, is unsafe
 only in interleavings where the waiting task starts early), so it can miss
-hazards the static checker proves; the test asks for zero false accepts:
-no schedule this oracle finds unsafe may be accepted by the checker.
+hazards the static checker proves; half the sampled runs are therefore
+adversarial (slow producers, eager consumers).  The test asks for zero false
+accepts: no schedule this oracle finds unsafe may be accepted by the checker.
+
+``find_cycle`` is an independent depth-first search for a cycle in the
+ordering graph (queue order plus counter edges), compared with the
+library's Kahn-based check on random task graphs.
+
+Pinned by hand-built schedules whose verdict is known by construction (a
+safe one, a cross-queue deadlock, an unsatisfiable wait, a race, a partial
+wait, a double write, a missing output, a self wait and a longer cycle) in
+the soundness tests.
 """
 from __future__ import annotations
 
@@ -258,8 +268,34 @@ def _inline_index(tasks: List[Task]) -> Dict[int, List[int]]:
     return by_ctr
 
 
-def simulate(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, rng: random.Random) -> Optional[str]:
-    """One random execution; a reason it went wrong, or None."""
+# Element states of the simulated buffers: an input nobody writes, a value
+# whose writer has not started, one being written, one written.
+_INPUT, _PENDING, _RUNNING, _DONE = 0, 1, 2, 3
+
+
+def _check_writes_once(acc) -> Optional[str]:
+    """A value written by two tasks of the schedule, or None."""
+    owner: Dict[str, Dict[int, int]] = {}
+    for i, (_, wr) in enumerate(acc):
+        for buf, lo, hi in wr:
+            d = owner.setdefault(buf, {})
+            for e in range(lo, hi):
+                if e in d:
+                    return f"{buf}[{e}] written by tasks {d[e]} and {i}"
+                d[e] = i
+    return None
+
+
+def simulate(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, rng: random.Random,
+             eager: float = 0.0) -> Optional[str]:
+    """One random execution; a reason it went wrong, or None.  Each step picks
+    one enabled action (start a queue's ready head task, or finish a running
+    task) uniformly.  With `eager` > 0 the run is adversarial: a random third
+    of the tasks are slow (they finish only when nothing else can happen),
+    and with probability `eager` a step picks among the starts only, when
+    there are any; consumers then start as early as their waits allow while
+    some producers are still running, which exposes a too-weak wait in fewer
+    runs.  Every execution sampled either way is one the device can perform."""
     n_lm = sum(1 for t in tasks if t.op == LMHEAD)
     queues: Dict[int, List[int]] = {}
     for i, t in enumerate(tasks):
@@ -269,53 +305,44 @@ def simulate(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, rng: rando
         q.sort(key=lambda i: tasks[i].seq)
     inline_of = _inline_index(tasks)
     acc = [accesses(s, t, n_lm) for t in tasks]
+    err = _check_writes_once(acc)
+    if err:
+        return err
+    # every buffer a task touches, sized to the largest index touched, each
+    # element INPUT until some task is found to write it (then PENDING)
+    size: Dict[str, int] = {}
+    for rd, wr in acc:
+        for buf, lo, hi in rd + wr:
+            size[buf] = max(size.get(buf, 0), hi)
+    state = {buf: bytearray(n) for buf, n in size.items()}
+    for _, wr in acc:
+        for buf, lo, hi in wr:
+            state[buf][lo:hi] = bytes([_PENDING]) * (hi - lo)
     counters = [0] * n_counters
     head = {c: 0 for c in queues}
     running: Dict[int, int] = {}  # queue -> task running on it
     done = [False] * len(tasks)
-    written: Dict[str, Dict[int, int]] = {}  # buffer -> element -> writer task
-    finished_writes: Dict[str, set] = {}
     inline_run = set()
+    slow = set(rng.sample(range(len(tasks)), len(tasks) // 3)) if eager else set()
 
     def ready(i):
         return all(counters[c] >= k for c, k in tasks[i].waits)
 
     def start_reads(i):
         for buf, lo, hi in acc[i][0]:
-            fin = finished_writes.get(buf, set())
-            for e in range(lo, hi):
-                w = written.get(buf, {}).get(e)
-                if w is not None and e not in fin:
-                    return f"task {i} reads {buf}[{e}] while writer {w} runs"
-                if w is None and _produced_later(buf, e):
-                    return f"task {i} reads {buf}[{e}] before it is written"
+            st = state[buf]
+            for bad, what in ((_RUNNING, "while its writer runs"), (_PENDING, "before it is written")):
+                e = st.find(bad, lo, hi)
+                if e >= 0:
+                    return f"task {i} reads {buf}[{e}] {what}"
         return None
 
-    producers_of: Dict[str, Dict[int, int]] = {}
-    for i, (rd, wr) in enumerate(acc):
-        for buf, lo, hi in wr:
-            d = producers_of.setdefault(buf, {})
-            for e in range(lo, hi):
-                if e in d:
-                    return f"{buf}[{e}] written by tasks {d[e]} and {i}"
-                d[e] = i
-
-    def _produced_later(buf, e):
-        return e in producers_of.get(buf, {})
-
-    def claim_writes(i):
+    def set_writes(i, val):
         for buf, lo, hi in acc[i][1]:
-            d = written.setdefault(buf, {})
-            for e in range(lo, hi):
-                d[e] = i
-
-    def finish_writes(i):
-        for buf, lo, hi in acc[i][1]:
-            f = finished_writes.setdefault(buf, set())
-            f.update(range(lo, hi))
+            state[buf][lo:hi] = bytes([val]) * (hi - lo)
 
     def finish(i):
-        finish_writes(i)
+        set_writes(i, _DONE)
         done[i] = True
         t = tasks[i]
         if t.signal >= 0:
@@ -333,8 +360,7 @@ def simulate(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, rng: rando
                     err = start_reads(j)
                     if err:
                         return err
-                    claim_writes(j)
-                    finish_writes(j)
+                    set_writes(j, _DONE)
                     done[j] = True
                 counters[t.chain] += 1
         return None
@@ -348,13 +374,19 @@ def simulate(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, rng: rando
                 actions.append(("start", c))
         if not actions:
             break
+        if slow:
+            fast = [a for a in actions if a[0] == "start" or running[a[1]] not in slow]
+            actions = fast or actions
+        starts = [a for a in actions if a[0] == "start"]
+        if starts and eager and rng.random() < eager:
+            actions = starts
         kind, c = rng.choice(actions)
         if kind == "start":
             i = queues[c][head[c]]
             err = start_reads(i)
             if err:
                 return err
-            claim_writes(i)
+            set_writes(i, _RUNNING)
             running[c] = i
         else:
             i = running.pop(c)
@@ -370,10 +402,67 @@ def simulate(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, rng: rando
     for l in range(s.L):
         if f"o{l}" not in read_bufs:  # the tiny schedule computes attention inside the O tasks
             req.pop(f"o{l}", None)
-    for buf, size in req.items():
-        have = finished_writes.get(buf, set())
-        if len(have) != size or (have and (min(have) != 0 or max(have) != size - 1)):
-            return f"{buf}: {len(have)} of {size} values written"
+    for buf, n in req.items():
+        st = state.get(buf, bytearray())
+        have = st[:n].count(_DONE) if len(st) >= n else st.count(_DONE)
+        if len(st) != n or have != n:
+            return f"{buf}: {have} of {n} values written"
+    return None
+
+
+def find_cycle(tasks: List[Task]) -> Optional[List[int]]:
+    """A cycle of the schedule's ordering graph (task indices), or None.
+
+    Edges: each queued task to the next one on its queue, and every task
+    that signals a counter to every task waiting on that counter (a wait
+    completes only after all of the counter's producers ran).  Iterative
+    depth-first search with three colours; independent of the library's
+    Kahn-based check."""
+    n = len(tasks)
+    succ: List[List[int]] = [[] for _ in range(n)]
+    by_queue: Dict[int, List[int]] = {}
+    for i, t in enumerate(tasks):
+        if t.cu != INLINE:
+            by_queue.setdefault(t.cu, []).append(i)
+    for q in by_queue.values():
+        q.sort(key=lambda i: tasks[i].seq)
+        for a, b in zip(q, q[1:]):
+            succ[a].append(b)
+    prod: Dict[int, List[int]] = {}
+    for i, t in enumerate(tasks):
+        if t.signal >= 0:
+            prod.setdefault(t.signal, []).append(i)
+    for i, t in enumerate(tasks):
+        for c, _ in t.waits:
+            for p in prod.get(c, []):
+                succ[p].append(i)
+    WHITE, GREY, BLACK = 0, 1, 2
+    colour = [WHITE] * n
+    parent = [-1] * n
+    for root in range(n):
+        if colour[root] != WHITE:
+            continue
+        stack = [(root, 0)]
+        colour[root] = GREY
+        while stack:
+            v, k = stack[-1]
+            if k < len(succ[v]):
+                stack[-1] = (v, k + 1)
+                w = succ[v][k]
+                if colour[w] == WHITE:
+                    colour[w] = GREY
+                    parent[w] = v
+                    stack.append((w, 0))
+                elif colour[w] == GREY:
+                    cyc = [w]
+                    u = v
+                    while u != w:
+                        cyc.append(u)
+                        u = parent[u]
+                    return cyc[::-1]
+            else:
+                colour[v] = BLACK
+                stack.pop()
     return None
 
 
@@ -383,8 +472,9 @@ def label(s: Shape, tasks: List[Task], n_cu: int, n_counters: int, runs: int = 8
     if why:
         return why
     rng = random.Random(seed)
-    for _ in range(runs):
-        why = simulate(s, tasks, n_cu, n_counters, rng)
+    for r in range(runs):
+        # alternate uniform interleavings with eager-start ones
+        why = simulate(s, tasks, n_cu, n_counters, rng, eager=0.9 if r % 2 else 0.0)
         if why:
             return why
     return None

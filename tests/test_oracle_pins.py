@@ -327,6 +327,19 @@ def test_int4_decode_equals_bf16_decode_on_representable_weights():
 
 
 # ---------------------------------------------------------------- argmax
+def test_top2_margin_hand_values():
+    """The reported greedy margin: largest minus second-largest logit, so a tie
+    gives 0 and the margin ignores order and all but the top two values."""
+    assert oracle.top2_margin(np.array([1.0, 3.0, 2.0])) == 1.0
+    assert oracle.top2_margin(np.array([-5.0, 0.25, -0.5, 0.0])) == 0.25
+    assert oracle.top2_margin(np.array([7.0, 7.0, 1.0])) == 0.0
+    assert oracle.top2_margin(np.array([2.0, -1.0])) == 3.0
+    v = np.random.default_rng(3).standard_normal(1000)
+    a, b = sorted(v)[-2:]
+    assert oracle.top2_margin(v) == b - a
+    assert oracle.top2_margin(v[::-1]) == b - a
+
+
 def test_argmax_ties_lowest_index_and_nan():
     assert oracle.argmax_first(np.array([1.0, 3.0, 3.0, 2.0])) == 1
     with pytest.raises(FloatingPointError):
