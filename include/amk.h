@@ -54,7 +54,9 @@ enum {
   AMK_ERR_COOPERATIVE_UNSUPPORTED = -6, /* no cooperative launch, or too few co-resident workgroups */
   AMK_ERR_TIMEOUT = -7,               /* a device-side counter wait exceeded its deadline (sticky) */
   AMK_ERR_BAD_STATE = -8,             /* handle in an error state; call amk_reset() */
-  AMK_ERR_ABORTED = -9                /* the host abort flag stopped a launch (sticky) */
+  AMK_ERR_ABORTED = -9,               /* the host abort flag stopped a launch (sticky) */
+  AMK_ERR_NONFINITE = -10             /* a logit of the step was NaN: its next token is meaningless
+                                         (sticky, like AMK_ERR_TIMEOUT) */
 };
 
 enum { AMK_WEIGHTS_BF16 = 0, AMK_WEIGHTS_W8A16 = 1, AMK_WEIGHTS_W4A16 = 2 };
@@ -143,8 +145,9 @@ typedef struct amk_handle_s* amk_handle_t;
  * the schedule tables, counters, scratch activations and the RoPE table.
  * Weight pointers are BORROWED: they must stay valid and unchanged until
  * amk_destroy(); nothing is copied or repacked.  tuning may be NULL.
- * Both schedule variants (AMK_SCHEDULE_SHORT / _LONG) are built and checked;
- * each step runs the one its position selects (amk_tuning_t.short_context).
+ * All three schedule variants (AMK_SCHEDULE_TINY, _SHORT and _LONG) are built
+ * and checked; each step runs the one its position selects
+ * (amk_tuning_t.tiny_context and .short_context).
  * On failure *out is set to NULL and nothing stays allocated. */
 int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
                amk_handle_t* out);
@@ -160,10 +163,15 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
  *             step never share a line with rows another workgroup reads)
  *   logits:   device pointer, 16-byte aligned, fp32 [vocab]
  * Errors: AMK_ERR_INVALID_ARGUMENT for token outside [0, vocab), pos outside
- * [0, max_seq) or a misaligned pointer; a sticky device error of an earlier step (AMK_ERR_TIMEOUT /
- * AMK_ERR_ABORTED, visible once that step finished) is returned and nothing
- * is launched until amk_reset().  One handle must not be driven from two
- * streams at once. */
+ * [0, max_seq), a misaligned pointer, or a kv_cache / logits pointer that is
+ * not device memory of the handle's device (host, pinned or another
+ * device's memory is refused before any launch); a sticky device error of an
+ * earlier step (AMK_ERR_TIMEOUT / AMK_ERR_ABORTED / AMK_ERR_NONFINITE,
+ * visible once that step finished) is returned and nothing is launched until
+ * amk_reset().  One handle must not be driven from two streams at once: a
+ * step enqueued on a different stream than the previous one while that
+ * stream still has work pending returns AMK_ERR_BAD_STATE and launches
+ * nothing (synchronise the old stream before switching). */
 int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, float* logits,
                     void* stream);
 
@@ -183,7 +191,7 @@ const int32_t* amk_next_token_ptr(amk_handle_t h);
 int amk_copy_next_token(amk_handle_t h, int32_t* dst, void* stream);
 
 /* Synchronise the handle's last stream and return its sticky device status
- * (AMK_OK, AMK_ERR_TIMEOUT, AMK_ERR_ABORTED). */
+ * (AMK_OK, AMK_ERR_TIMEOUT, AMK_ERR_ABORTED, AMK_ERR_NONFINITE). */
 int amk_get_status(amk_handle_t h);
 
 /* Clear a sticky error: waits for the device, zeroes the counters and

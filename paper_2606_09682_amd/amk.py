@@ -25,6 +25,7 @@ AMK_ERR_COOPERATIVE_UNSUPPORTED = -6
 AMK_ERR_TIMEOUT = -7
 AMK_ERR_BAD_STATE = -8
 AMK_ERR_ABORTED = -9
+AMK_ERR_NONFINITE = -10
 
 AMK_WEIGHTS_BF16 = 0
 AMK_WEIGHTS_W8A16 = 1
@@ -332,6 +333,9 @@ class Decoder:
                 setattr(lw, field, lin(p + name, quant))
         lm = amk_linear_t(None, None) if cfg.tied_embeddings else lin("lm_head", quant)
         self._weights = amk_weights_t(ptr("embed"), ptr("final_norm"), lm, self._layers)
+        import torch
+        # the device amk_create resolved (-1 = the current device at creation)
+        self._dev = cfg.device if cfg.device >= 0 else torch.cuda.current_device()
         self.handle = amk_create(cfg, self._weights, tuning)
 
     def kv_cache_bytes(self) -> int:
@@ -342,7 +346,10 @@ class Decoder:
         tensors of at least amk_kv_cache_bytes and 4 * vocab bytes."""
         if not hasattr(self, "_need"):
             self._need = (amk_kv_cache_bytes(self.cfg), 4 * self.cfg.vocab)
+        dev = self._dev
         for t, need, what in ((kv_cache, self._need[0], "kv_cache"), (logits, self._need[1], "logits")):
+            if not t.is_cuda or t.device.index != dev:
+                raise ValueError(f"{what} must be a tensor on cuda:{dev}, the decoder's device")
             if not t.is_contiguous() or t.numel() * t.element_size() < need:
                 raise ValueError(f"{what} must be contiguous with at least {need} bytes")
         if stream is None:

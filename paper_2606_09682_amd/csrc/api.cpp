@@ -51,9 +51,16 @@ struct amk_handle_s {
   void* d_block = nullptr;      // one device allocation for tables and scratch
   int32_t* h_status = nullptr;  // host-mapped
   int32_t* h_abort = nullptr;   // host-mapped
+  uint32_t* h_done = nullptr;   // host-mapped: number of the last launch whose argmax finished
   void* last_stream = nullptr;
   bool launched = false;
+  uint32_t launch_seq = 0;      // launches enqueued so far
   uint64_t timeout_ticks = 0;
+  // the last kv_cache / logits pointers found to be device memory of this
+  // device with room for a step's accesses (the check is skipped while the
+  // caller keeps passing them)
+  const void* ok_kv = nullptr;
+  const void* ok_logits = nullptr;
 };
 
 namespace {
@@ -82,6 +89,8 @@ int check_linear(const amk_linear_t& l, int fmt) {
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+size_t amk_kv_cache_bytes_of(const Shape& s) { return (size_t)s.L * 2 * s.nkv * (size_t)s.max_seq * s.hd * 2; }
+
 void free_handle(amk_handle_s* h) {
   if (!h) return;
   DeviceGuard g(h->device);
@@ -89,7 +98,27 @@ void free_handle(amk_handle_s* h) {
   if (h->d_block) (void)hipFree(h->d_block);
   if (h->h_status) (void)hipHostFree(h->h_status);
   if (h->h_abort) (void)hipHostFree(h->h_abort);
+  if (h->h_done) (void)hipHostFree(h->h_done);
   delete h;
+}
+
+// Whether [p, p + bytes) lies inside one allocation of device memory on
+// `device` (not host, pinned host or another device's memory).
+bool device_range(const void* p, size_t bytes, int device) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (a.type != hipMemoryTypeDevice || a.device != device) return false;
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  const uintptr_t b = (uintptr_t)base, q = (uintptr_t)p;
+  return q >= b && bytes <= size && q - b <= size - bytes;
 }
 
 }  // namespace
@@ -108,6 +137,7 @@ const char* amk_status_string(int status) {
     case AMK_ERR_TIMEOUT: return "device counter wait timed out";
     case AMK_ERR_BAD_STATE: return "handle in an error state";
     case AMK_ERR_ABORTED: return "launch aborted by the host abort flag";
+    case AMK_ERR_NONFINITE: return "a logit was NaN";
     default: return "unknown status";
   }
 }
@@ -115,7 +145,7 @@ const char* amk_status_string(int status) {
 size_t amk_kv_cache_bytes(const amk_config_t* cfg) {
   Shape s;
   if (amk::derive_shape(cfg, nullptr, 1, &s, nullptr) != AMK_OK) return 0;
-  return (size_t)s.L * 2 * s.nkv * (size_t)s.max_seq * s.hd * 2;
+  return amk_kv_cache_bytes_of(s);
 }
 
 int amk_schedule_size(const amk_config_t* cfg, const amk_tuning_t* tuning, int32_t n_cu, int32_t variant,
@@ -346,16 +376,21 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     if (hipHostMalloc((void**)&h->h_status, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
             hipSuccess ||
         hipHostMalloc((void**)&h->h_abort, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+            hipSuccess ||
+        hipHostMalloc((void**)&h->h_done, sizeof(uint32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
             hipSuccess) {
       free_handle(h);
       return AMK_ERR_OUT_OF_MEMORY;
     }
     *(volatile int32_t*)h->h_status = 0;
     *(volatile int32_t*)h->h_abort = 0;
+    *(volatile uint32_t*)h->h_done = 0;
     int32_t* d_status = nullptr;
     int32_t* d_hab = nullptr;
+    uint32_t* d_done = nullptr;
     if (hipHostGetDevicePointer((void**)&d_status, h->h_status, 0) != hipSuccess ||
-        hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess) {
+        hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess ||
+        hipHostGetDevicePointer((void**)&d_done, h->h_done, 0) != hipSuccess) {
       free_handle(h);
       return AMK_ERR_DEVICE;
     }
@@ -428,6 +463,7 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     m.dev_abort = (int32_t*)(base + r_abort.off);
     m.host_status = d_status;
     m.host_abort = d_hab;
+    m.host_done = d_done;
     for (int v = 0; v < kVariants; ++v) {
       h->dsch[v].tasks = (const amk_task_t*)(base + r_tasks[v].off);
       h->dsch[v].queue_start = (const int32_t*)(base + r_queue[v].off);
@@ -459,8 +495,20 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   if (((uintptr_t)kv_cache & 255u) != 0 || !aligned16(logits)) return AMK_ERR_INVALID_ARGUMENT;
   const int sticky = *(volatile int32_t*)h->h_status;
   if (sticky != 0) return sticky;
+  // another stream while the previous step has not finished: the two steps
+  // would share the handle's counters and scratch
+  if (h->launched && stream != h->last_stream && *(volatile uint32_t*)h->h_done != h->launch_seq)
+    return AMK_ERR_BAD_STATE;
   DeviceGuard guard(h->device);
   if (!guard.ok) return AMK_ERR_DEVICE;
+  if (kv_cache != h->ok_kv) {
+    if (!device_range(kv_cache, amk_kv_cache_bytes_of(h->s), h->device)) return AMK_ERR_INVALID_ARGUMENT;
+    h->ok_kv = kv_cache;
+  }
+  if (logits != h->ok_logits) {
+    if (!device_range(logits, sizeof(float) * (size_t)h->s.V, h->device)) return AMK_ERR_INVALID_ARGUMENT;
+    h->ok_logits = logits;
+  }
   const int variant = pos + 1 <= h->s.tiny_context    ? AMK_SCHEDULE_TINY
                       : pos + 1 <= h->s.short_context ? AMK_SCHEDULE_SHORT
                                                       : AMK_SCHEDULE_LONG;
@@ -470,6 +518,7 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   m.queue_start = ds.queue_start;
   m.trace = ds.trace;
   m.counters = ds.counters;
+  m.launch_seq = h->launch_seq + 1;
   const uint32_t epoch = ds.epoch + 1;  // counter targets are epoch * producers, mod 2^32
   const int st = amk_internal_launch(&m, variant == AMK_SCHEDULE_TINY, token, pos, epoch, (uint16_t*)kv_cache, logits,
                                      h->timeout_ticks, stream);
@@ -478,6 +527,7 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   ds.epoch = epoch;
   h->last_stream = stream;
   h->launched = true;
+  h->launch_seq = m.launch_seq;
   return AMK_OK;
 }
 
@@ -517,6 +567,7 @@ int amk_reset(amk_handle_t h) {
   if (hipMemset(h->dm.dev_abort, 0, sizeof(int32_t)) != hipSuccess) return AMK_ERR_DEVICE;
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
   *(volatile int32_t*)h->h_status = 0;
+  *(volatile uint32_t*)h->h_done = h->launch_seq;  // a stopped launch never reported its end
   return AMK_OK;
 }
 

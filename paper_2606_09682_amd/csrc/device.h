@@ -67,6 +67,8 @@ struct DevModel {
   int32_t* dev_abort;        // device word: nonzero stops every workgroup at its next wait
   int32_t* host_status;      // host-mapped: first device error code
   const int32_t* host_abort; // host-mapped: raised by amk_set_abort
+  uint32_t* host_done;       // host-mapped: launch_seq of the last launch whose argmax finished
+  uint32_t launch_seq;       // number of this launch on its handle (1, 2, ...)
   // schedule of this launch (one of the handle's variants)
   uint64_t* trace;           // [n_tasks][AMK_TRACE_FIELDS] timestamps, or null
   const amk_task_t* tasks;   // sorted by (cu, seq)

@@ -40,8 +40,9 @@
 // Every result another workgroup reads is stored coherent at agent scope
 // (write-through past the XCD's L2), so releasing it takes only a drain of
 // the storing wave's own stores before the counter increment: no L2
-// writeback.  Only the sync wave waits on counters (acquire: invalidate,
-// then plain loads) and increments them; streaming waves never drain while
+// writeback.  Only the sync wave waits on counters (acquire: agent-scope
+// polls, then plain loads with no cache invalidation, see
+// acquire_after_poll) and increments them; streaming waves never drain while
 // their weight loads are in flight.
 // Lane reductions use DPP (VALU latency) rather than LDS permutes.
 //
@@ -522,6 +523,13 @@ __device__ __forceinline__ void consume_block(const uint4 (&buf)[N], const uint3
 //  - the launch's own acquire has invalidated every cached copy of earlier
 //    launches' data;
 //  - no cache line holds parts of two such vectors (256-byte strides).
+// Producers' row ranges are not line-aligned: several producers, often on
+// different XCDs, write parts of one 128-byte line.  This relies on the L2
+// keeping written-through bytes with a byte mask: a store does not make the
+// rest of its line valid, so a later read of the line by a CU of that XCD
+// fetches the other producers' bytes from memory.  (The SmolLM2-shaped
+// decoder, whose residual tasks own 2 or 3 rows, puts up to 16 producers in
+// one line and decodes 32 greedy steps in agreement with the oracle.)
 // So a line a workgroup finds in its L1 or its XCD's L2 was fetched after the
 // producers had released all of it, and the XCD's L2 serves one fetch of an
 // input vector to all its CUs instead of one per CU.  The fence only keeps
@@ -833,18 +841,25 @@ __device__ __forceinline__ void epi_gateup(const DevModel& m, const amk_task_t& 
   }
 }
 
-// LM head: logits + per-task argmax partial (lowest index on ties).
+// LM head: logits + per-task argmax partial (lowest index on ties).  A NaN
+// logit never wins a comparison; it records the sticky status
+// AMK_ERR_NONFINITE, so the step's next token is reported as meaningless
+// instead of silently skipping it.
 __device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& t, const Gemv& g, const Lds& L,
                                            float rs, float* logits, int lane) {
   float best = -INFINITY;
   int besti = 0x7fffffff;
+  bool nan = false;
   const Ranges wr = wave_ranges(g);
   for (int r = t.begin + lane; r < t.end; r += 64) {
     float y = row_sum(L.part, m.part_stride, g, wr, r - t.begin) * rs;
     if (g.int8) y *= L.stat[r - t.begin];
     stc(logits + r, y);
+    nan |= y != y;
     if (y > best || (y == best && r < besti)) { best = y; besti = r; }
   }
+  if (__any(nan) && lane == 0)
+    __hip_atomic_store(m.host_status, (int32_t)AMK_ERR_NONFINITE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float ob = __shfl_xor(best, o);
@@ -868,7 +883,11 @@ __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t
     const int oi = __shfl_xor(besti, o);
     if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
   }
-  if (lane == 0) stc(m.next_token, besti);
+  if (lane == 0) {
+    stc(m.next_token, besti);
+    // every other task of the step happens before this one: the step is done
+    __hip_atomic_store(m.host_done, m.launch_seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
 }
 
 // ---------------------------------------------------------------- attention (all 8 waves)

@@ -56,7 +56,7 @@ int main(void) {
   O(amk_task_t, signal_counter) O(amk_task_t, chain_counter) O(amk_check_report_t, message)
   E(AMK_ABI_VERSION) E(AMK_OK) E(AMK_ERR_INVALID_ARGUMENT) E(AMK_ERR_UNSUPPORTED) E(AMK_ERR_SCHEDULE_REJECTED)
   E(AMK_ERR_OUT_OF_MEMORY) E(AMK_ERR_DEVICE) E(AMK_ERR_COOPERATIVE_UNSUPPORTED) E(AMK_ERR_TIMEOUT)
-  E(AMK_ERR_BAD_STATE) E(AMK_ERR_ABORTED) E(AMK_WEIGHTS_BF16) E(AMK_WEIGHTS_W8A16) E(AMK_WEIGHTS_W4A16)
+  E(AMK_ERR_BAD_STATE) E(AMK_ERR_ABORTED) E(AMK_ERR_NONFINITE) E(AMK_WEIGHTS_BF16) E(AMK_WEIGHTS_W8A16) E(AMK_WEIGHTS_W4A16)
   E(AMK_MAX_WAITS)
   E(AMK_OP_QKV) E(AMK_OP_ATTN) E(AMK_OP_COMBINE) E(AMK_OP_O) E(AMK_OP_GATEUP) E(AMK_OP_DOWN) E(AMK_OP_LMHEAD)
   E(AMK_OP_ARGMAX) E(AMK_CHECK_OK) E(AMK_CHECK_WELL_FORMED) E(AMK_CHECK_CAPACITY) E(AMK_CHECK_WAIT_SATISFIABLE)
@@ -99,7 +99,7 @@ def test_ctypes_mirror_matches_header():
 
 
 def test_status_strings(lib):
-    for code in range(0, -10, -1):
+    for code in range(0, -11, -1):
         assert amk.amk_status_string(code) not in ("", "unknown status")
     assert amk.amk_status_string(-99) == "unknown status"
 

@@ -264,6 +264,216 @@ def test_8b_positions(amk, torch_cuda, fmt):
             compare(f"llama3_8b {variant}", fmt, g, o, pos)
 
 
+def planted_lm_head(w, fmt, rows):
+    """A copy of `w` whose untied LM head has the given rows replaced by one
+    and the same single-entry row: a power of two (exact in bf16), signed like
+    the final normalised hidden state at its largest entry, in that entry's
+    column.  Any summation order gives those rows the same logit bit for bit,
+    on both sides, and it is about twice the largest logit of the random rows,
+    so the step's greedy token is decided by the tie rule alone.  (No larger:
+    the planted weight multiplies the hidden state's own reassociation error
+    into the logit, like any weight.)  The other tensors are shared with `w`."""
+    import copy
+    cfg = w.cfg
+    assert not cfg.tied_embeddings
+    model = oracle.OracleModel(w, fmt, np.float32, cache=False)
+    trace = {}
+    kv = synth.make_kv_cache(cfg, 0, max_seq=2)
+    logits0 = oracle.decode_step(model, 1, 0, kv, trace=trace)
+    hf = oracle.rmsnorm(trace["x"][-1], model.vec("final_norm"), cfg.rms_eps)
+    k = int(np.argmax(np.abs(hf)))
+    value = 2.0 ** np.ceil(np.log2(2.0 * np.max(np.abs(logits0)) / abs(float(hf[k]))))
+    row = np.zeros(cfg.hidden, np.float32)
+    row[k] = np.float32(np.sign(hf[k]) * value)
+    bits = synth.f32_to_bf16_bits(row)
+    p = copy.copy(w)
+    p.bf16 = dict(w.bf16)
+    lm = w.bf16["lm_head"].copy()
+    lm[list(rows)] = bits
+    p.bf16["lm_head"] = lm
+    p.q8, p.scale, p.q4, p.scale4 = dict(w.q8), dict(w.scale), dict(w.q4), dict(w.scale4)
+    if fmt == "w8a16":
+        p.q8["lm_head"], p.scale["lm_head"] = synth.quantize_rows(lm)
+    if fmt == "w4a16":
+        p.q4["lm_head"], p.scale4["lm_head"] = synth.quantize_groups4(lm, w.group4)
+    return p
+
+
+def lm_task_rows(cfg, n_cu):
+    """Row ranges of the LM-head tasks of the lowering (their order)."""
+    from paper_2606_09682_amd import amk as amk_mod
+    c = amk_mod.make_config(**config_kwargs(cfg, "bf16", 4))
+    tasks, _ = amk_mod.amk_schedule_export(c, n_cu, variant=amk_mod.AMK_SCHEDULE_TINY)
+    return sorted((t.begin, t.end) for t in tasks if t.op == amk_mod.AMK_OP_LMHEAD)
+
+
+def tie_pairs(cfg, n_cu):
+    """Pairs of LM-head rows that tie: in two different tasks, in one task on
+    two lanes of the epilogue, and (for tasks of more than 64 rows) on one
+    lane in two passes of the epilogue loop."""
+    r = lm_task_rows(cfg, n_cu)
+    (b0, e0), (b1, e1) = r[1], r[len(r) * 3 // 4]
+    pairs = {"two tasks": (b0 + 1, b1 + 2), "two lanes": (b0 + 1, b0 + 5)}
+    big = [(b, e) for b, e in r if e - b > 64]
+    if big:
+        b, e = big[len(big) // 2]
+        pairs["one lane"] = (b + 3, b + 67)
+    return pairs
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_argmax_ties_tiny(amk, torch_cuda, fmt):
+    """Equal maximal logits at two vocabulary rows: the greedy token is the
+    lower index (paper-silent reading: first occurrence), wherever the two rows
+    sit among the LM-head tasks and their epilogue lanes."""
+    w = weights_for(tiny_shape(fmt), fmt=fmt)
+    cfg = w.cfg
+    n_cu = torch_cuda.cuda.get_device_properties(0).multi_processor_count
+    for where, (i, j) in tie_pairs(cfg, n_cu).items():
+        p = planted_lm_head(w, fmt, (i, j))
+        kv = synth.make_kv_cache(cfg, 0, max_seq=4)
+        o = oracle_decode(p, fmt, 0, 1, kv)
+        assert o[0] == [i] and o[1][0][i] == o[1][0][j], (where, o[0])
+        g = gpu_decode(amk, torch_cuda, p, fmt, 0, 1, kv, 4)
+        say(f"tie {where}: rows {i}, {j}: gpu token {g[0]}")
+        assert g[1][0][i] == g[1][0][j]
+        compare(f"tiny tie {where}", fmt, g, o, 0)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+def test_argmax_ties_8b(amk, torch_cuda, fmt):
+    """The tie rule on the Llama-3-8B shape (501-row LM-head tasks): two
+    tasks, two lanes, and one lane in two passes of the epilogue loop."""
+    w = weights_for("llama3_8b", fmt=fmt)
+    cfg = w.cfg
+    n_cu = torch_cuda.cuda.get_device_properties(0).multi_processor_count
+    pairs = tie_pairs(cfg, n_cu)
+    rows = sorted({r for pr in pairs.values() for r in pr})
+    # all three pairs at once: six equal rows, the lowest index wins
+    p = planted_lm_head(w, fmt, rows)
+    kv = synth.make_kv_cache(cfg, 0, max_seq=2)
+    o = oracle_decode(p, fmt, 0, 1, kv)
+    assert o[0] == [rows[0]]
+    g = gpu_decode(amk, torch_cuda, p, fmt, 0, 1, kv, 2)
+    assert len({float(g[1][0][r]) for r in rows}) == 1
+    compare(f"llama3_8b ties {pairs}", fmt, g, o, 0)
+
+
+def test_nan_logit_is_reported(amk, torch_cuda):
+    """A NaN logit (an LM-head row of NaN weights) is not skipped silently:
+    the step records the sticky AMK_ERR_NONFINITE, later steps return it until
+    reset, and after a reset the handle decodes normally."""
+    import copy
+    import torch
+    w = weights_for("tiny")
+    cfg = w.cfg
+    p = copy.copy(w)
+    p.bf16 = dict(w.bf16)
+    lm = w.bf16["lm_head"].copy()
+    lm[123] = 0x7FC0  # bf16 quiet NaN
+    p.bf16["lm_head"] = lm
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", 4)), weights_to_device(p, "bf16"))
+    kv = kv_to_device(synth.make_kv_cache(cfg, 0, max_seq=4))
+    logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+    dec.step(1, 0, kv, logits)
+    assert dec.status() == amk.AMK_ERR_NONFINITE
+    assert torch.isnan(logits[123]).item() and torch.isfinite(logits[:123]).all().item()
+    with pytest.raises(amk.AmkError) as e:
+        dec.step(1, 1, kv, logits)
+    assert e.value.status == amk.AMK_ERR_NONFINITE
+    dec.reset()
+    assert dec.status() == amk.AMK_OK
+    dec.close()
+
+
+def test_pointer_checks(amk, torch_cuda):
+    """kv_cache / logits that are not device memory of the decoder's device
+    are refused before any launch: by the binding (CPU tensors) and by the C
+    library itself (host and pinned host pointers passed straight through the
+    C ABI)."""
+    import torch
+    w = weights_for("tiny")
+    cfg = w.cfg
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", 16)), weights_to_device(w, "bf16"))
+    nkv = amk.amk_kv_cache_bytes(dec.cfg)
+    kv = torch.zeros(nkv // 2, dtype=torch.int16, device="cuda")
+    logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+    with pytest.raises(ValueError):
+        dec.step(1, 0, kv.cpu(), logits)
+    with pytest.raises(ValueError):
+        dec.step(1, 0, kv, logits.cpu())
+    host_kv = torch.zeros(nkv // 2 + 128, dtype=torch.int16).pin_memory()
+    off = (-host_kv.data_ptr()) % 256 // 2
+    stream = torch.cuda.current_stream().cuda_stream
+    for kv_ptr, lg_ptr in ((host_kv.data_ptr() + 2 * off, logits.data_ptr()),
+                           (kv.data_ptr(), torch.empty(cfg.vocab, dtype=torch.float32).pin_memory().data_ptr())):
+        with pytest.raises(amk.AmkError) as e:
+            amk.amk_decode_step(dec.handle, 1, 0, kv_ptr, lg_ptr, stream)
+        assert e.value.status == amk.AMK_ERR_INVALID_ARGUMENT
+    dec.step(1, 0, kv, logits)
+    assert dec.status() == amk.AMK_OK
+    dec.close()
+
+
+def test_second_stream_while_busy(amk, torch_cuda):
+    """A step enqueued on another stream while the handle's previous step has
+    not finished is refused with AMK_ERR_BAD_STATE (nothing launched); once
+    the first stream is done, switching streams works and decodes correctly."""
+    import torch
+    w = weights_for("tiny")
+    cfg = w.cfg
+    kv_np = synth.make_kv_cache(cfg, 0)
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, "bf16", cfg.seq_capacity)), weights_to_device(w, "bf16"))
+    kv = kv_to_device(kv_np)
+    logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        torch.cuda._sleep(50_000_000)  # keeps s1 busy for milliseconds at least
+        dec.step(1, 0, kv, logits, stream=s1.cuda_stream)
+    with pytest.raises(amk.AmkError) as e:
+        dec.step(1, 1, kv, logits, stream=s2.cuda_stream)
+    assert e.value.status == amk.AMK_ERR_BAD_STATE
+    s1.synchronize()
+    t0 = dec.next_token(stream=s1.cuda_stream)
+    dec.step(t0, 1, kv, logits, stream=s2.cuda_stream)
+    t1 = dec.next_token(stream=s2.cuda_stream)
+    assert dec.status() == amk.AMK_OK
+    dec.close()
+    o = oracle_decode(w, "bf16", 0, 2, kv_np)
+    assert [t0, t1] == o[0]
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "w8a16"])
+def test_repeatable_across_handles(amk, torch_cuda, fmt):
+    """The step is deterministic: 32 greedy steps of the SmolLM2 shape (whose
+    2- and 3-row residual tasks put many producers on one cache line) give
+    bit-identical logits and KV rows on two handles and on a second run of the
+    first handle."""
+    w = weights_for("smollm2_135m", fmt=fmt)
+    cfg = w.cfg
+    kv = synth.make_kv_cache(cfg, 0)
+    runs = [gpu_decode(amk, torch_cuda, w, fmt, 0, cfg.greedy_steps, kv, cfg.seq_capacity) for _ in range(2)]
+    import torch
+    dec = amk.Decoder(amk.make_config(**config_kwargs(cfg, fmt, cfg.seq_capacity)), weights_to_device(w, fmt))
+    for rep in range(2):
+        kvd = kv_to_device(kv)
+        logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+        toks, lg = [], []
+        t = 1
+        for i in range(cfg.greedy_steps):
+            dec.step(t, i, kvd, logits)
+            t = dec.next_token()
+            toks.append(t)
+            lg.append(logits.cpu().numpy().astype(np.float64))
+        runs.append((toks, lg, kv_from_device(kvd)))
+    dec.close()
+    for r in runs[1:]:
+        assert r[0] == runs[0][0]
+        assert all(np.array_equal(a, b) for a, b in zip(r[1], runs[0][1]))
+        assert np.array_equal(r[2], runs[0][2])
+
+
 @pytest.mark.parametrize("group", [32, 64, 256])
 def test_w4a16_group_sizes(amk, torch_cuda, group):
     """int4 scales over 32 .. 256 columns (one to eight lanes' 32-column blocks
