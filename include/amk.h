@@ -178,6 +178,35 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
 /* Synchronise the device, free everything the handle owns.  NULL is a no-op. */
 int amk_destroy(amk_handle_t h);
 
+/* ---- no-allocation variant --------------------------------------------------- */
+
+/* Bytes of the library's static device array that amk_create_static uses. */
+#define AMK_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code running under HIP
+ * graph capture, serving loops and harnesses that forbid hipMalloc): the same
+ * handle as amk_create, with the same checks, schedules and kernels, but all
+ * the device memory the handle owns (task tables, counters, activations, the
+ * RoPE table and the status words) lives in one static device array of
+ * AMK_STATIC_SCRATCH_BYTES per device, which every process that uses the
+ * library on a device holds until it ends.  Calls no hipMalloc, hipHostMalloc
+ * or hipFree (the schedule is built in ordinary host memory and copied in with
+ * hipMemcpy; the array is cleared with hipMemset).
+ * Limits: a model whose tables and scratch need more than
+ * AMK_STATIC_SCRATCH_BYTES (the Llama-3-8B shape with an 8194-position cache
+ * needs about 35 MiB) fails with AMK_ERR_OUT_OF_MEMORY and a message on stderr.  One
+ * array per device holds one handle: while a static handle lives, another
+ * amk_create_static on that device fails with AMK_ERR_BAD_STATE; destroy the
+ * first one before creating the next (the new handle clears what it uses;
+ * two handles would race on the same counters and scratch).  Because the
+ * status words are device memory, amk_decode_step on a static handle does not
+ * return an earlier step's sticky error (amk_get_status, which waits for the
+ * stream, does), does not detect use from two streams, and amk_set_abort
+ * returns AMK_ERR_UNSUPPORTED; every counter wait is still bounded by the
+ * deadline.  amk_destroy and every other function work as for amk_create. */
+int amk_create_static(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
+                      amk_handle_t* out);
+
 /* ---- helpers --------------------------------------------------------------- */
 
 /* Bytes of the KV cache amk_decode_step expects for cfg (0 for an invalid cfg). */

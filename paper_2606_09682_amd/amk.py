@@ -111,6 +111,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "amk_create": (ctypes.c_int, [P(amk_config_t), P(amk_weights_t), P(amk_tuning_t), P(ctypes.c_void_p)]),
         "amk_decode_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                            ctypes.c_void_p, ctypes.c_void_p]),
+        "amk_create_static": (ctypes.c_int, [P(amk_config_t), P(amk_weights_t), P(amk_tuning_t),
+                                             P(ctypes.c_void_p)]),
         "amk_destroy": (ctypes.c_int, [ctypes.c_void_p]),
         "amk_kv_cache_bytes": (ctypes.c_size_t, [P(amk_config_t)]),
         "amk_next_token_ptr": (ctypes.c_void_p, [ctypes.c_void_p]),
@@ -157,6 +159,15 @@ def amk_create(cfg: amk_config_t, weights: amk_weights_t, tuning: Optional[amk_t
     h = ctypes.c_void_p()
     _check(load().amk_create(ctypes.byref(cfg), ctypes.byref(weights), ctypes.byref(tuning) if tuning else None,
                              ctypes.byref(h)), "amk_create")
+    return h
+
+
+def amk_create_static(cfg: amk_config_t, weights: amk_weights_t,
+                      tuning: Optional[amk_tuning_t] = None) -> ctypes.c_void_p:
+    """amk_create whose device memory is the library's static array (see amk.h)."""
+    h = ctypes.c_void_p()
+    _check(load().amk_create_static(ctypes.byref(cfg), ctypes.byref(weights),
+                                    ctypes.byref(tuning) if tuning else None, ctypes.byref(h)), "amk_create_static")
     return h
 
 
@@ -295,9 +306,11 @@ class Decoder:
     under the same name + '.scale', or, for W4A16, packed uint8 [out, in/2]
     with an fp16 [out, in/group] scale tensor under name + '.scale'.  The
     tensors are borrowed: they must
-    outlive the decoder, which keeps references to them."""
+    outlive the decoder, which keeps references to them.  ``static=True``
+    creates the handle with amk_create_static (no device allocation)."""
 
-    def __init__(self, cfg: amk_config_t, tensors: Mapping[str, "object"], tuning: Optional[amk_tuning_t] = None):
+    def __init__(self, cfg: amk_config_t, tensors: Mapping[str, "object"], tuning: Optional[amk_tuning_t] = None,
+                 static: bool = False):
         self.cfg = cfg
         check_sizes(cfg, tensors)
         self._keep: Dict[str, object] = dict(tensors)
@@ -336,7 +349,7 @@ class Decoder:
         import torch
         # the device amk_create resolved (-1 = the current device at creation)
         self._dev = cfg.device if cfg.device >= 0 else torch.cuda.current_device()
-        self.handle = amk_create(cfg, self._weights, tuning)
+        self.handle = (amk_create_static if static else amk_create)(cfg, self._weights, tuning)
 
     def kv_cache_bytes(self) -> int:
         return amk_kv_cache_bytes(self.cfg)

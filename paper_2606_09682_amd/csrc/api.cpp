@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -23,6 +24,7 @@ using amk::amk_internal_launch;
 using amk::amk_internal_occupancy;
 using amk::amk_internal_prepare;
 using amk::amk_internal_read_probe;
+using amk::amk_internal_static_scratch;
 using amk::amk_internal_threads;
 
 constexpr int kVariants = 3;
@@ -52,6 +54,10 @@ struct amk_handle_s {
   int32_t* h_status = nullptr;  // host-mapped
   int32_t* h_abort = nullptr;   // host-mapped
   uint32_t* h_done = nullptr;   // host-mapped: number of the last launch whose argmax finished
+  // amk_create_static: the device block is the library's static scratch
+  // array, and the status / abort / done words are device words in it
+  bool is_static = false;
+  int32_t* d_words = nullptr;   // static handles: status at [0], abort at [16], done at [32]
   void* last_stream = nullptr;
   bool launched = false;
   uint32_t launch_seq = 0;      // launches enqueued so far
@@ -91,11 +97,30 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 size_t amk_kv_cache_bytes_of(const Shape& s) { return (size_t)s.L * 2 * s.nkv * (size_t)s.max_seq * s.hd * 2; }
 
+// The live handle of each device whose device memory is the static scratch
+// array (at most one: the array holds one handle's tables and scratch).
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+amk_handle_s* g_static_owner[kMaxDevices] = {};
+
+bool claim_static(int device, amk_handle_s* h) {
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (device < 0 || device >= kMaxDevices || g_static_owner[device]) return false;
+  g_static_owner[device] = h;
+  return true;
+}
+
+void release_static(int device, amk_handle_s* h) {
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (device >= 0 && device < kMaxDevices && g_static_owner[device] == h) g_static_owner[device] = nullptr;
+}
+
 void free_handle(amk_handle_s* h) {
   if (!h) return;
   DeviceGuard g(h->device);
   if (h->launched) (void)hipDeviceSynchronize();
-  if (h->d_block) (void)hipFree(h->d_block);
+  if (h->is_static) release_static(h->device, h);
+  else if (h->d_block) (void)hipFree(h->d_block);
   if (h->h_status) (void)hipHostFree(h->h_status);
   if (h->h_abort) (void)hipHostFree(h->h_abort);
   if (h->h_done) (void)hipHostFree(h->h_done);
@@ -234,7 +259,10 @@ int amk_check_config(const amk_config_t* cfg, int32_t n_cu) {
   }
 }
 
-int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning, amk_handle_t* out) {
+// amk_create and amk_create_static: `use_static` puts every byte of device
+// memory the handle owns into the static scratch array (no allocation).
+static int create_impl(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
+                       amk_handle_t* out, bool use_static) {
   if (!out) return AMK_ERR_INVALID_ARGUMENT;
   *out = nullptr;
   if (!cfg || !w) return AMK_ERR_INVALID_ARGUMENT;
@@ -355,6 +383,8 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
     const Region r_argp = take(sizeof(float) * 2 * n_lm);
     const Region r_next = take(sizeof(int32_t));
     const Region r_abort = take(sizeof(int32_t));
+    // static handles: status, abort and done words, each on its own 64 bytes
+    const Region r_words = take(use_static ? 3 * 64 : 0);
     const bool tracing = tuning && tuning->trace;
     Region r_tasks[kVariants], r_queue[kVariants], r_trace[kVariants], r_ctr[kVariants];
     for (int v = 0; v < kVariants; ++v) {
@@ -363,36 +393,65 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
       r_queue[v] = take(sizeof(int32_t) * h->sch[v].queue_start.size());
       r_trace[v] = take(tracing ? sizeof(uint64_t) * AMK_TRACE_FIELDS * h->sch[v].tasks.size() : 0);
     }
-    if (hipMalloc(&h->d_block, top) != hipSuccess) {
+    if (use_static) {
+      void* sp = nullptr;
+      size_t cap = 0;
+      if (amk::amk_internal_static_scratch(dev, &sp, &cap) != AMK_OK) {
+        free_handle(h);
+        return AMK_ERR_DEVICE;
+      }
+      if (top > cap) {
+        std::fprintf(stderr, "amk: amk_create_static needs %zu bytes of device memory, the static scratch holds %zu\n",
+                     top, cap);
+        free_handle(h);
+        return AMK_ERR_OUT_OF_MEMORY;
+      }
+      if (!claim_static(dev, h)) {
+        std::fprintf(stderr, "amk: device %d already has a live amk_create_static handle\n", dev);
+        free_handle(h);
+        return AMK_ERR_BAD_STATE;
+      }
+      h->is_static = true;
+      h->d_block = sp;
+    } else if (hipMalloc(&h->d_block, top) != hipSuccess) {
       h->d_block = nullptr;
       free_handle(h);
       return AMK_ERR_OUT_OF_MEMORY;
     }
     char* base = (char*)h->d_block;
+    // zeroes the counters, the scratch and (static handles) the status words:
+    // the static array keeps whatever the previous handle left in it
     if (hipMemset(h->d_block, 0, top) != hipSuccess) {
       free_handle(h);
       return AMK_ERR_DEVICE;
     }
-    if (hipHostMalloc((void**)&h->h_status, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
-            hipSuccess ||
-        hipHostMalloc((void**)&h->h_abort, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
-            hipSuccess ||
-        hipHostMalloc((void**)&h->h_done, sizeof(uint32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
-            hipSuccess) {
-      free_handle(h);
-      return AMK_ERR_OUT_OF_MEMORY;
-    }
-    *(volatile int32_t*)h->h_status = 0;
-    *(volatile int32_t*)h->h_abort = 0;
-    *(volatile uint32_t*)h->h_done = 0;
     int32_t* d_status = nullptr;
     int32_t* d_hab = nullptr;
     uint32_t* d_done = nullptr;
-    if (hipHostGetDevicePointer((void**)&d_status, h->h_status, 0) != hipSuccess ||
-        hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess ||
-        hipHostGetDevicePointer((void**)&d_done, h->h_done, 0) != hipSuccess) {
-      free_handle(h);
-      return AMK_ERR_DEVICE;
+    if (use_static) {
+      h->d_words = (int32_t*)(base + r_words.off);
+      d_status = h->d_words;
+      d_hab = h->d_words + 16;
+      d_done = (uint32_t*)(h->d_words + 32);
+    } else {
+      if (hipHostMalloc((void**)&h->h_status, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+              hipSuccess ||
+          hipHostMalloc((void**)&h->h_abort, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+              hipSuccess ||
+          hipHostMalloc((void**)&h->h_done, sizeof(uint32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+              hipSuccess) {
+        free_handle(h);
+        return AMK_ERR_OUT_OF_MEMORY;
+      }
+      *(volatile int32_t*)h->h_status = 0;
+      *(volatile int32_t*)h->h_abort = 0;
+      *(volatile uint32_t*)h->h_done = 0;
+      if (hipHostGetDevicePointer((void**)&d_status, h->h_status, 0) != hipSuccess ||
+          hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess ||
+          hipHostGetDevicePointer((void**)&d_done, h->h_done, 0) != hipSuccess) {
+        free_handle(h);
+        return AMK_ERR_DEVICE;
+      }
     }
 
     // host-built tables
@@ -489,16 +548,29 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
   }
 }
 
+int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning, amk_handle_t* out) {
+  return create_impl(cfg, w, tuning, out, false);
+}
+
+int amk_create_static(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
+                      amk_handle_t* out) {
+  return create_impl(cfg, w, tuning, out, true);
+}
+
 int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, float* logits, void* stream) {
   if (!h || !kv_cache || !logits) return AMK_ERR_INVALID_ARGUMENT;
   if (token < 0 || token >= h->s.V || pos < 0 || pos >= h->s.max_seq) return AMK_ERR_INVALID_ARGUMENT;
   if (((uintptr_t)kv_cache & 255u) != 0 || !aligned16(logits)) return AMK_ERR_INVALID_ARGUMENT;
-  const int sticky = *(volatile int32_t*)h->h_status;
-  if (sticky != 0) return sticky;
-  // another stream while the previous step has not finished: the two steps
-  // would share the handle's counters and scratch
-  if (h->launched && stream != h->last_stream && *(volatile uint32_t*)h->h_done != h->launch_seq)
-    return AMK_ERR_BAD_STATE;
+  // (a static handle's status words are device memory: reading them would
+  // wait for the device, so neither check is made for it)
+  if (!h->is_static) {
+    const int sticky = *(volatile int32_t*)h->h_status;
+    if (sticky != 0) return sticky;
+    // another stream while the previous step has not finished: the two steps
+    // would share the handle's counters and scratch
+    if (h->launched && stream != h->last_stream && *(volatile uint32_t*)h->h_done != h->launch_seq)
+      return AMK_ERR_BAD_STATE;
+  }
   DeviceGuard guard(h->device);
   if (!guard.ok) return AMK_ERR_DEVICE;
   if (kv_cache != h->ok_kv) {
@@ -553,6 +625,11 @@ int amk_get_status(amk_handle_t h) {
   if (!h) return AMK_ERR_INVALID_ARGUMENT;
   DeviceGuard guard(h->device);
   if (h->launched && hipStreamSynchronize((hipStream_t)h->last_stream) != hipSuccess) return AMK_ERR_DEVICE;
+  if (h->is_static) {
+    int32_t v = 0;
+    if (hipMemcpy(&v, h->d_words, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return AMK_ERR_DEVICE;
+    return v;
+  }
   return *(volatile int32_t*)h->h_status;
 }
 
@@ -565,9 +642,12 @@ int amk_reset(amk_handle_t h) {
     ds.epoch = 0;
   }
   if (hipMemset(h->dm.dev_abort, 0, sizeof(int32_t)) != hipSuccess) return AMK_ERR_DEVICE;
+  if (h->is_static && hipMemset(h->d_words, 0, sizeof(int32_t)) != hipSuccess) return AMK_ERR_DEVICE;
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
-  *(volatile int32_t*)h->h_status = 0;
-  *(volatile uint32_t*)h->h_done = h->launch_seq;  // a stopped launch never reported its end
+  if (!h->is_static) {
+    *(volatile int32_t*)h->h_status = 0;
+    *(volatile uint32_t*)h->h_done = h->launch_seq;  // a stopped launch never reported its end
+  }
   return AMK_OK;
 }
 
@@ -588,6 +668,7 @@ int amk_trace_copy(amk_handle_t h, uint64_t* dst, int64_t capacity, int32_t* n_t
 
 int amk_set_abort(amk_handle_t h, int32_t value) {
   if (!h) return AMK_ERR_INVALID_ARGUMENT;
+  if (h->is_static) return AMK_ERR_UNSUPPORTED;  // its abort word is device memory
   __atomic_store_n(h->h_abort, value ? 1 : 0, __ATOMIC_SEQ_CST);
   return AMK_OK;
 }

@@ -3,6 +3,7 @@
 // argument, so every field is a wave-uniform kernel-argument load.
 #pragma once
 
+#include <cstddef>
 #include <cstdint>
 
 #include "../../include/amk.h"
@@ -92,5 +93,8 @@ extern "C" int amk_internal_attn_scratch(int group, int head_dim);
 extern "C" int amk_internal_prepare(int head_dim, int group, int fmt, int lds_bytes);
 extern "C" int amk_internal_occupancy(int head_dim, int group, int fmt, int lds_bytes, int* blocks_per_cu);
 extern "C" int amk_internal_read_probe(const void* buf, int64_t bytes, int32_t blocks, uint32_t* sink, void* stream);
+// Device address and size of the static scratch array on `device`, which the
+// caller has made current (looked up once per device, then cached).
+extern "C" int amk_internal_static_scratch(int device, void** ptr, size_t* bytes);
 
 }  // namespace amk

@@ -50,6 +50,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "device.h"
 #include "schedule.h"
@@ -1525,6 +1526,33 @@ extern "C" int amk_internal_read_probe(const void* buf, int64_t bytes, int32_t b
   hipLaunchKernelGGL(amk_read_kernel, dim3(blocks), dim3(NT), 0, (hipStream_t)stream, (const uint4*)buf, bytes / 16,
                      sink);
   return hipGetLastError() == hipSuccess ? AMK_OK : AMK_ERR_DEVICE;
+}
+
+// ---------------------------------------------------------------- static scratch
+// Device memory of a handle made by amk_create_static (its task tables,
+// counters, activations, RoPE table and status words): one array per device,
+// held from the library's first use on that device until the process ends.
+// In host code `scratch` only names the array; its device address on each
+// device comes from hipGetSymbolAddress and is used everywhere instead.
+static __device__ __align__(256) unsigned char scratch[AMK_STATIC_SCRATCH_BYTES];
+
+extern "C" int amk_internal_static_scratch(int device, void** ptr, size_t* bytes) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  if (!ptr || !bytes || device < 0 || device >= kMaxDevices) return AMK_ERR_INVALID_ARGUMENT;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return AMK_ERR_DEVICE;
+    }
+    addr[device] = p;
+  }
+  *ptr = addr[device];
+  *bytes = sizeof(scratch);
+  return AMK_OK;
 }
 
 // ---------------------------------------------------------------- host side
