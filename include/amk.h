@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define AMK_ABI_VERSION 4
+#define AMK_ABI_VERSION 5
 
 /* ---- status codes ------------------------------------------------------ */
 enum {
@@ -130,7 +130,17 @@ typedef struct {
                                (AMK_SCHEDULE_SHORT); 0 = 256; negative = never */
   int32_t tiny_context;     /* steps with pos + 1 <= tiny_context (at most AMK_TINY_MAX) run the
                                tiny-context schedule (AMK_SCHEDULE_TINY); 0 = 6; negative = never */
+  int32_t queue_assign;     /* how the tasks of a stage are placed on the CU queues (paper §4,
+                               ScheduleConfig sm_assignment): AMK_ASSIGN_ROUND_ROBIN (0) or
+                               AMK_ASSIGN_LPT (1) */
 } amk_tuning_t;
+
+/* amk_tuning_t.queue_assign.  ROUND_ROBIN: task i of a stage of n tasks goes to
+ * queue i mod n_cu (stages narrower than the grid start where the previous
+ * narrow stage stopped).  LPT (longest processing time first): the tasks of a
+ * stage, largest estimated cost first (bytes streamed plus a fixed per-task
+ * cost), each go to the queue with the least estimated work so far. */
+enum { AMK_ASSIGN_ROUND_ROBIN = 0, AMK_ASSIGN_LPT = 1 };
 
 /* Largest tiny_context: the tiny schedule's attention keeps every position in registers. */
 #define AMK_TINY_MAX 8

@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libamk.so")
 
 # ---- constants (mirror include/amk.h) ---------------------------------------
-AMK_ABI_VERSION = 4
+AMK_ABI_VERSION = 5
 AMK_OK = 0
 AMK_ERR_INVALID_ARGUMENT = -1
 AMK_ERR_UNSUPPORTED = -2
@@ -32,6 +32,7 @@ AMK_WEIGHTS_W8A16 = 1
 AMK_WEIGHTS_W4A16 = 2
 
 AMK_SCHEDULE_SHORT, AMK_SCHEDULE_LONG, AMK_SCHEDULE_TINY = 0, 1, 2
+AMK_ASSIGN_ROUND_ROBIN, AMK_ASSIGN_LPT = 0, 1
 AMK_TINY_MAX = 8
 AMK_OP_QKV, AMK_OP_ATTN, AMK_OP_COMBINE, AMK_OP_O, AMK_OP_GATEUP, AMK_OP_DOWN, AMK_OP_LMHEAD, AMK_OP_ARGMAX = range(1, 9)
 AMK_MAX_WAITS = 4
@@ -71,7 +72,7 @@ class amk_weights_t(ctypes.Structure):
 class amk_tuning_t(ctypes.Structure):
     _fields_ = [("attn_splits", ctypes.c_int32), ("timeout_us", ctypes.c_int32),
                 ("max_rows_per_task", ctypes.c_int32), ("trace", ctypes.c_int32), ("short_context", ctypes.c_int32),
-                ("tiny_context", ctypes.c_int32)]
+                ("tiny_context", ctypes.c_int32), ("queue_assign", ctypes.c_int32)]
 
 
 class amk_task_t(ctypes.Structure):

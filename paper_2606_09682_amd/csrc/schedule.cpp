@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <numeric>
+#include <queue>
 
 namespace amk {
 
@@ -108,6 +109,12 @@ int derive_shape(const amk_config_t* cfg, const amk_tuning_t* tuning, int n_cu, 
     return AMK_ERR_INVALID_ARGUMENT;
   }
   s->tiny_context = tc == 0 ? kDefaultTinyContext : tc < 0 ? 0 : tc;
+  const int qa = tuning ? tuning->queue_assign : AMK_ASSIGN_ROUND_ROBIN;
+  if (qa != AMK_ASSIGN_ROUND_ROBIN && qa != AMK_ASSIGN_LPT) {
+    set_msg(why, "queue_assign %ld unknown", qa);
+    return AMK_ERR_INVALID_ARGUMENT;
+  }
+  s->assign = qa;
   return AMK_OK;
 }
 
@@ -169,6 +176,39 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
   auto n_tasks = [&](int items, int jobs_per_item) { return stage_tasks(items, jobs_per_item, n_cu, s.max_jobs); };
   auto cu_of = [&](int i, int n) { return n >= n_cu ? i % n_cu : (rot + i) % n_cu; };
   auto bump = [&](int n) { if (n < n_cu) rot = (rot + n) % n_cu; };
+  // LPT: estimated work per queue so far, in bytes streamed; a task costs
+  // the bytes of its weight rows (or K/V rows) plus a fixed per-task cost
+  // for its wait, input load and epilogue (about 2.5 us of streaming)
+  const bool lpt = s.assign == AMK_ASSIGN_LPT;
+  std::vector<double> load(n_cu, 0.0);
+  constexpr double kTaskFixedBytes = 64.0 * 1024;
+  const double wbytes = s.fmt == AMK_WEIGHTS_BF16 ? 2.0 : s.fmt == AMK_WEIGHTS_W8A16 ? 1.0 : 0.5;
+  // queues for the n tasks of one stage with per-task costs `cost`
+  auto place = [&](const std::vector<double>& cost) {
+    const int n = (int)cost.size();
+    std::vector<int> cu(n);
+    if (!lpt) {
+      for (int i = 0; i < n; ++i) cu[i] = cu_of(i, n);
+      bump(n);
+      return cu;
+    }
+    std::vector<int> idx(n);
+    std::iota(idx.begin(), idx.end(), 0);
+    std::stable_sort(idx.begin(), idx.end(), [&](int a, int b) { return cost[a] > cost[b]; });
+    // least-loaded queue first, lowest index on ties
+    using Item = std::pair<double, int>;
+    std::priority_queue<Item, std::vector<Item>, std::greater<Item>> heap;
+    for (int c = 0; c < n_cu; ++c) heap.push({load[c], c});
+    for (int i : idx) {
+      const Item it = heap.top();
+      heap.pop();
+      cu[i] = it.second;
+      load[it.second] = it.first + cost[i] + kTaskFixedBytes;
+      heap.push({load[it.second], it.second});
+    }
+    return cu;
+  };
+  auto gemv_cost = [&](int rows, int in) { return rows * (double)in * wbytes; };
   auto lo = [](int total, int parts, int i) { return (int)((long)total * i / parts); };
   // A stage's n producers signal kStageCounters counters (task i counter i mod
   // k), and its consumers wait on each with that counter's producer count:
@@ -188,9 +228,12 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
     const int n = n_tasks(items, jobs_per_item);
     int first = 0;
     const Waits out = stage_counters(n, &first);
+    const int in = op == AMK_OP_O ? s.nq * s.hd : op == AMK_OP_DOWN ? s.I : s.H;
+    std::vector<double> cost(n);
+    for (int i = 0; i < n; ++i) cost[i] = gemv_cost((lo(items, n, i + 1) - lo(items, n, i)) * jobs_per_item, in);
+    const std::vector<int> cu = place(cost);
     for (int i = 0; i < n; ++i)
-      add(op, layer, cu_of(i, n), lo(items, n, i), lo(items, n, i + 1), 0, w, sig_of(first, n, i));
-    bump(n);
+      add(op, layer, cu[i], lo(items, n, i), lo(items, n, i + 1), 0, w, sig_of(first, n, i));
     return out;
   };
 
@@ -209,22 +252,27 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
       n_ctr += s.nkv;
     }
     const int c_done = tinyv ? -1 : n_ctr++;  // every KV group's attention output is written
+    std::vector<double> qcost(n_qkv);
+    for (int k = 0; k < n_qkv; ++k)
+      qcost[k] = gemv_cost(2 * (lo(s.gunits, s.npg, k % s.npg + 1) - lo(s.gunits, s.npg, k % s.npg)), s.H);
+    const std::vector<int> qcu = place(qcost);
     for (int g = 0; g < s.nkv; ++g) {
       for (int i = 0; i < s.npg; ++i) {
         const int b = g * s.gunits + lo(s.gunits, s.npg, i), e = g * s.gunits + lo(s.gunits, s.npg, i + 1);
-        add(AMK_OP_QKV, l, cu_of(g * s.npg + i, n_qkv), b, e, g, prev,
+        add(AMK_OP_QKV, l, qcu[g * s.npg + i], b, e, g, prev,
             tinyv ? sig_of(c_qkv0, n_qkv, g * s.npg + i) : c_qkv0 + g, shortv ? c_done : -1);
       }
     }
-    bump(n_qkv);
     if (tinyv) {
       // O tasks compute the attention themselves from q and the KV cache
       const int n = n_tasks(s.H, 1);
       int first = 0;
       const Waits o_out = stage_counters(n, &first);
+      std::vector<double> ocost(n);
+      for (int i = 0; i < n; ++i) ocost[i] = gemv_cost(lo(s.H, n, i + 1) - lo(s.H, n, i), s.nq * s.hd);
+      const std::vector<int> ocu = place(ocost);
       for (int i = 0; i < n; ++i)
-        add(AMK_OP_O, l, cu_of(i, n), lo(s.H, n, i), lo(s.H, n, i + 1), 1, qkv_out, sig_of(first, n, i));
-      bump(n);
+        add(AMK_OP_O, l, ocu[i], lo(s.H, n, i), lo(s.H, n, i + 1), 1, qkv_out, sig_of(first, n, i));
       const Waits gu = stage(AMK_OP_GATEUP, l, s.I, 2, o_out);
       prev = stage(AMK_OP_DOWN, l, s.H, 1, gu);
       continue;
@@ -240,12 +288,13 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
       const int c_grp0 = n_ctr;
       n_ctr += s.nkv;
       const int n_attn = s.nkv * s.nsplit;
+      // a split's K/V rows are not known when the schedule is built (they
+      // grow with the position): equal nominal costs
+      const std::vector<int> acu = place(std::vector<double>(n_attn, 2.0 * s.hd * 2 * 256));
       for (int i = 0; i < n_attn; ++i) {
         const int g = i / s.nsplit;
-        add(AMK_OP_ATTN, l, cu_of(i, n_attn), i % s.nsplit, s.nsplit, g, {{c_qkv0 + g, s.npg}}, c_grp0 + g,
-            c_done);
+        add(AMK_OP_ATTN, l, acu[i], i % s.nsplit, s.nsplit, g, {{c_qkv0 + g, s.npg}}, c_grp0 + g, c_done);
       }
-      bump(n_attn);
       for (int g = 0; g < s.nkv; ++g)
         add(AMK_OP_COMBINE, l, AMK_CU_INLINE, g * s.group, (g + 1) * s.group, g, {{c_grp0 + g, s.nsplit}}, c_done);
     }
@@ -258,10 +307,13 @@ Schedule build_schedule(const Shape& s, int n_cu, int variant) {
     const int n = n_tasks(s.V, 1);
     int first = 0;
     const Waits lm_out = stage_counters(n, &first);
+    const double lm_bytes = s.tied ? 2.0 : wbytes;
+    std::vector<double> lcost(n);
+    for (int i = 0; i < n; ++i) lcost[i] = (lo(s.V, n, i + 1) - lo(s.V, n, i)) * (double)s.H * lm_bytes;
+    const std::vector<int> lcu = place(lcost);
     for (int i = 0; i < n; ++i)
-      add(AMK_OP_LMHEAD, 0, cu_of(i, n), lo(s.V, n, i), lo(s.V, n, i + 1), i, prev, sig_of(first, n, i));
-    bump(n);
-    add(AMK_OP_ARGMAX, 0, cu_of(0, 1), 0, n, 0, lm_out, -1);
+      add(AMK_OP_LMHEAD, 0, lcu[i], lo(s.V, n, i), lo(s.V, n, i + 1), i, prev, sig_of(first, n, i));
+    add(AMK_OP_ARGMAX, 0, place({0.0})[0], 0, n, 0, lm_out, -1);
     sch.n_lm_slots = n;
   }
   sch.n_counters = n_ctr;

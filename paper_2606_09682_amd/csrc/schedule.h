@@ -34,6 +34,7 @@ struct Shape {
   int max_jobs = 0;      // GEMV rows per task cap
   int short_context = 0; // steps with pos + 1 <= short_context use the short schedule
   int tiny_context = 0;  // steps with pos + 1 <= tiny_context use the tiny schedule
+  int assign = 0;        // AMK_ASSIGN_ROUND_ROBIN or AMK_ASSIGN_LPT
   float theta = 0.f, eps = 0.f;
 };
 

@@ -1,10 +1,13 @@
 """Knob search for one decode workload: the schedule knobs of amk_tuning_t
-(attention splits, rows per task, the short / tiny schedule crossovers) are
-tried one at a time around the current best, each candidate
+(attention splits, rows per task, the short / tiny schedule crossovers, the
+round-robin or LPT queue assignment) are tried one at a time around the
+current best, each candidate
 
-* gated on correctness: same greedy token and logits within 2e-2 of the
-  current best configuration's on the same inputs (whose own correctness the
-  GPU parity tests establish against the CPU oracle),
+* gated on correctness against the CPU oracle: the same greedy token and
+  every logit within 2e-2 of the oracle's result for the same inputs, read
+  from the file ``python -m oracle.reference`` writes (the search never runs
+  the oracle itself); the default configuration must pass the same gate
+  before anything is timed,
 * timed paired and interleaved with the current best (A, B, A, B, ...
   launches on one stream, per-pair time ratios, median and p10 / p90), so a
   clock ramp affects both alike,
@@ -13,7 +16,8 @@ tried one at a time around the current best, each candidate
 * kept only if the median ratio is below 1 - min_gain (paper §3, the
   propose -> evaluate -> keep / revert loop, here without an agent).
 
-    python -m paper_2606_09682_amd.tune --config llama3_8b --fmt bf16 --pos 1024
+    python -m oracle.reference --config llama3_8b --fmt bf16 --pos 1024 --out ref.npz
+    python -m paper_2606_09682_amd.tune --config llama3_8b --fmt bf16 --pos 1024 --reference ref.npz
 
 Prints one JSON line per candidate and a final line with the best tuning.
 Seeded synthetic weights and KV cache of the named shape; one GPU.
@@ -33,7 +37,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-KNOBS = ("attn_splits", "max_rows_per_task", "short_context", "tiny_context")
+KNOBS = ("attn_splits", "max_rows_per_task", "short_context", "tiny_context", "queue_assign")
+TOL = 2e-2
 
 
 def tuning_of(amk, knobs: Dict[str, int]):
@@ -54,7 +59,17 @@ def candidates(knob: str, cur: int, pos: int) -> List[int]:
         return [v for v in (-1, max(1, pos // 2), pos + 1, 2 * (pos + 1)) if v != cur]
     if knob == "tiny_context":
         return [v for v in (-1, 1, 2, 4, 6, 8) if v != cur]
+    if knob == "queue_assign":  # round robin (0, the default) or LPT (1)
+        return [v for v in (0, 1) if v != cur]
     return []
+
+
+def load_reference(path: str, workload: str):
+    """(token, logits) of the oracle for `workload` from an oracle.reference file."""
+    with np.load(path, allow_pickle=False) as z:
+        if str(z["workload"]) != workload:
+            raise ValueError(f"{path} holds {z['workload']}, the search runs {workload}")
+        return int(z["token"]), z["logits"].astype(np.float64)
 
 
 def paired(torch, dec_a, dec_b, step_a, step_b, pairs: int):
@@ -83,7 +98,11 @@ def main(argv: Optional[List[str]] = None) -> int:
     ap.add_argument("--pairs", type=int, default=30)
     ap.add_argument("--min-gain", type=float, default=0.005)
     ap.add_argument("--rounds", type=int, default=1)
+    ap.add_argument("--reference", required=True,
+                    help="the oracle's result for this workload (python -m oracle.reference ... --out FILE)")
     args = ap.parse_args(argv)
+    workload = f"{args.config}_{args.fmt}_pos{args.pos}"
+    tok_ref, lg_ref = load_reference(args.reference, workload)
 
     import torch
 
@@ -116,10 +135,18 @@ def main(argv: Optional[List[str]] = None) -> int:
         dec.step(1, args.pos, kv, logits)
         return dec.next_token(), logits.cpu().numpy()
 
+    def gate(tok, lg):
+        err = float(np.max(np.abs(lg.astype(np.float64) - lg_ref)))
+        return tok == tok_ref and err <= TOL, err
+
     best: Dict[str, int] = {}
     kv_best = kv_to_device(kv_np)
     dec_best = make(best)
-    tok_ref, lg_ref = run_once(dec_best, kv_best)
+    ok, err = gate(*run_once(dec_best, kv_best))
+    if not ok:
+        print(json.dumps({"knobs": best, "result": "baseline_wrong", "max_abs_logit_diff": err}), flush=True)
+        dec_best.close()
+        return 3
     for _ in range(args.rounds):
         for knob in KNOBS:
             for v in candidates(knob, best.get(knob, 0), args.pos):
@@ -132,8 +159,8 @@ def main(argv: Optional[List[str]] = None) -> int:
                     continue
                 kv = kv_to_device(kv_np)
                 tok, lg = run_once(dec, kv)
-                err = float(np.max(np.abs(lg.astype(np.float64) - lg_ref)))
-                if tok != tok_ref or not err <= 2e-2:
+                ok, err = gate(tok, lg)
+                if not ok:
                     rec.update(result="wrong", token=tok, ref_token=tok_ref, max_abs_logit_diff=err)
                     print(json.dumps(rec), flush=True)
                     dec.close()
@@ -159,7 +186,7 @@ def main(argv: Optional[List[str]] = None) -> int:
     logits = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
     ta, _ = paired(torch, dec_best, dec_best, lambda: dec_best.step(1, args.pos, kv_best, logits),
                    lambda: dec_best.step(1, args.pos, kv_best, logits), args.pairs)
-    print(json.dumps({"best": best, "workload": f"{args.config}_{args.fmt}_pos{args.pos}",
+    print(json.dumps({"best": best, "workload": workload,
                       "us_median": float(np.median(ta)), "floor_us": floor_us}), flush=True)
     dec_best.close()
     return 0

@@ -51,7 +51,7 @@ int main(void) {
   S(amk_check_report_t)
   O(amk_config_t, rope_theta) O(amk_config_t, device) O(amk_config_t, group_size) O(amk_layer_weights_t, down)
   O(amk_weights_t, layers)
-  O(amk_tuning_t, trace) O(amk_tuning_t, short_context) O(amk_tuning_t, tiny_context)
+  O(amk_tuning_t, trace) O(amk_tuning_t, short_context) O(amk_tuning_t, tiny_context) O(amk_tuning_t, queue_assign)
   O(amk_task_t, aux) O(amk_task_t, n_wait) O(amk_task_t, wait_counter) O(amk_task_t, wait_count)
   O(amk_task_t, signal_counter) O(amk_task_t, chain_counter) O(amk_check_report_t, message)
   E(AMK_ABI_VERSION) E(AMK_OK) E(AMK_ERR_INVALID_ARGUMENT) E(AMK_ERR_UNSUPPORTED) E(AMK_ERR_SCHEDULE_REJECTED)
@@ -64,7 +64,7 @@ int main(void) {
   E(AMK_CHECK_OUTPUT) E(AMK_CHECK_INLINE) E(AMK_CU_INLINE) E(AMK_TRACE_FIELDS) E(AMK_TRACE_WAIT_BEGIN) E(AMK_TRACE_WAIT_END) E(AMK_TRACE_INPUT_READY)
   E(AMK_TRACE_COMPUTE_END) E(AMK_TRACE_SIGNALLED) E(AMK_TRACE_PUBLISHED)
   E(AMK_TRACE_CHAINED) E(AMK_TRACE_SATISFIED) E(AMK_SCHEDULE_SHORT) E(AMK_SCHEDULE_LONG)
-  E(AMK_SCHEDULE_TINY) E(AMK_TINY_MAX)
+  E(AMK_SCHEDULE_TINY) E(AMK_TINY_MAX) E(AMK_ASSIGN_ROUND_ROBIN) E(AMK_ASSIGN_LPT)
   return 0;
 }
 '''

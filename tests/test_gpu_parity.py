@@ -36,7 +36,7 @@ def tuning_for(amk, variant=None, **kw):
     sc = {None: 0, "tiny": 0, "short": SHORT_ALWAYS, "long": LONG_ALWAYS}[variant]
     tc = {None: 0, "tiny": amk.AMK_TINY_MAX}.get(variant, -1)
     return amk.amk_tuning_t(kw.get("attn_splits", 0), kw.get("timeout_us", 0), kw.get("max_rows", 0),
-                            kw.get("trace", 0), sc, tc)
+                            kw.get("trace", 0), sc, tc, kw.get("queue_assign", 0))
 
 
 def say(msg):
@@ -472,6 +472,27 @@ def test_repeatable_across_handles(amk, torch_cuda, fmt):
         assert r[0] == runs[0][0]
         assert all(np.array_equal(a, b) for a, b in zip(r[1], runs[0][1]))
         assert np.array_equal(r[2], runs[0][2])
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("name", ["tiny", "smollm2_135m", "llama32_1b"])
+def test_lpt_assignment(amk, torch_cuda, name, fmt):
+    """Schedules lowered with the LPT queue assignment decode like the oracle:
+    greedy steps from position 0 (tiny schedule first) and a step at a filled
+    position under the long schedule."""
+    w = weights_for(tiny_shape(fmt) if name == "tiny" else name, fmt=fmt)
+    cfg = w.cfg
+    steps = 8 if name == "tiny" else 2
+    kv = synth.make_kv_cache(cfg, 0, max_seq=320)
+    o = oracle_decode(w, fmt, 0, steps, kv)
+    g = gpu_decode(amk, torch_cuda, w, fmt, 0, steps, kv, 320,
+                   tuning=tuning_for(amk, None, queue_assign=amk.AMK_ASSIGN_LPT))
+    compare(f"{cfg.name} lpt", fmt, g, o, 0)
+    kv = synth.make_kv_cache(cfg, 300, seed=1, max_seq=320)
+    o = oracle_decode(w, fmt, 300, 1, kv)
+    g = gpu_decode(amk, torch_cuda, w, fmt, 300, 1, kv, 320,
+                   tuning=tuning_for(amk, "long", queue_assign=amk.AMK_ASSIGN_LPT))
+    compare(f"{cfg.name} lpt long", fmt, g, o, 300)
 
 
 @pytest.mark.parametrize("group", [32, 64, 256])

@@ -468,3 +468,65 @@ def test_tiny_o_reading_unwritten_output_rejected(tiny_tiny):
     m[find(m, amk.AMK_OP_O, 1)].aux = 0
     rep = check(cfg, m, nc)
     assert not rep.ok and rep.rule == amk.AMK_CHECK_OUTPUT, rep.message
+
+
+# ---------------------------------------------------------------- LPT queue assignment
+def lpt_tuning():
+    t = amk.amk_tuning_t()
+    t.queue_assign = amk.AMK_ASSIGN_LPT
+    return t
+
+
+@pytest.mark.parametrize("name", list(synth.CONFIGS))
+@pytest.mark.parametrize("n_cu", [256, 13])
+@pytest.mark.parametrize("variant", [amk.AMK_SCHEDULE_SHORT, amk.AMK_SCHEDULE_LONG, amk.AMK_SCHEDULE_TINY])
+def test_lpt_lowering_accepted(lib, name, n_cu, variant):
+    """The longest-processing-time assignment (paper §4 ScheduleConfig
+    sm_assignment 'load_balance') lowers every config to a schedule the
+    checker accepts, with the same tasks as round robin on other queues."""
+    cfg = cfg_of(name, "w8a16")
+    t = lpt_tuning()
+    tasks, nc = amk.amk_schedule_export(cfg, n_cu, t, variant=variant)
+    rep = amk.amk_schedule_check(cfg, n_cu, tasks, nc, t)
+    assert rep.ok == 1, rep.message
+    rr, nc_rr = amk.amk_schedule_export(cfg, n_cu, variant=variant)
+    assert nc == nc_rr
+    key = lambda x: (x.op, x.layer, x.begin, x.end, x.aux)  # noqa: E731
+    assert sorted(map(key, tasks)) == sorted(map(key, rr))
+    assert amk.amk_check_config(cfg, n_cu) == amk.AMK_OK
+
+
+def _queue_loads(tasks, cfg, n_cu):
+    """Estimated work per queue: weight bytes of each GEMV task plus 64 KiB
+    per task (the cost model the LPT assignment is documented with)."""
+    wb = {amk.AMK_WEIGHTS_BF16: 2.0, amk.AMK_WEIGHTS_W8A16: 1.0}[cfg.weight_format]
+    H, I, qd = cfg.hidden, cfg.intermediate, cfg.n_heads * cfg.head_dim
+    load = [0.0] * n_cu
+    for t in tasks:
+        if t.cu == amk.AMK_CU_INLINE or t.op not in (amk.AMK_OP_QKV, amk.AMK_OP_O, amk.AMK_OP_GATEUP,
+                                                      amk.AMK_OP_DOWN, amk.AMK_OP_LMHEAD):
+            continue
+        rows = (t.end - t.begin) * (2 if t.op in (amk.AMK_OP_QKV, amk.AMK_OP_GATEUP) else 1)
+        k = qd if t.op == amk.AMK_OP_O else I if t.op == amk.AMK_OP_DOWN else H
+        b = 2.0 if (t.op == amk.AMK_OP_LMHEAD and cfg.tied_embeddings) else wb
+        load[t.cu] += rows * k * b + 65536
+    return load
+
+
+@pytest.mark.parametrize("name", ["tiny", "smollm2_135m", "tinyllama_1b"])
+def test_lpt_balances_at_least_as_well(lib, name):
+    """On 13 queues, where the stages do not divide evenly, the most loaded
+    queue carries no more estimated GEMV work under LPT than under round
+    robin."""
+    cfg = cfg_of(name)
+    lpt, _ = amk.amk_schedule_export(cfg, 13, lpt_tuning(), variant=amk.AMK_SCHEDULE_TINY)
+    rr, _ = amk.amk_schedule_export(cfg, 13, variant=amk.AMK_SCHEDULE_TINY)
+    assert max(_queue_loads(lpt, cfg, 13)) <= max(_queue_loads(rr, cfg, 13))
+
+
+def test_unknown_queue_assign_rejected(lib):
+    t = amk.amk_tuning_t()
+    t.queue_assign = 7
+    with pytest.raises(amk.AmkError) as e:
+        amk.amk_schedule_export(cfg_of("tiny"), 16, t)
+    assert e.value.status == amk.AMK_ERR_INVALID_ARGUMENT

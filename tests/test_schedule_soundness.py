@@ -57,12 +57,16 @@ VARIANTS = [amk.AMK_SCHEDULE_SHORT, amk.AMK_SCHEDULE_LONG, amk.AMK_SCHEDULE_TINY
 @pytest.mark.parametrize("name", ["tiny", "smollm2_135m"])
 @pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("n_cu", [16, 13])
-def test_real_lowerings_safe_and_accepted(lib, name, variant, n_cu):
+@pytest.mark.parametrize("assign", [amk.AMK_ASSIGN_ROUND_ROBIN, amk.AMK_ASSIGN_LPT])
+def test_real_lowerings_safe_and_accepted(lib, name, variant, n_cu, assign):
     cfg = cfg_of(name)
-    tasks, nc = amk.amk_schedule_export(cfg, n_cu, variant=variant)
+    tuning = amk.amk_tuning_t()
+    tuning.queue_assign = assign
+    tasks, nc = amk.amk_schedule_export(cfg, n_cu, tuning, variant=variant)
     s = shape_of(name, tasks)
     s.nsplit = max(1, min(64, n_cu // synth.get(name).n_kv_heads))
     assert sim.label(s, sim.from_descriptors(tasks), n_cu, nc, runs=4) is None
+    assert sim.find_cycle(sim.from_descriptors(tasks)) is None
     assert checker_accepts(cfg, tasks, nc, n_cu)
 
 
