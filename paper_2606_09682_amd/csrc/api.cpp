@@ -53,14 +53,13 @@ struct amk_handle_s {
   void* d_block = nullptr;      // one device allocation for tables and scratch
   int32_t* h_status = nullptr;  // host-mapped
   int32_t* h_abort = nullptr;   // host-mapped
-  uint32_t* h_done = nullptr;   // host-mapped: number of the last launch whose argmax finished
   // amk_create_static: the device block is the library's static scratch
   // array, and the status / abort / done words are device words in it
   bool is_static = false;
-  int32_t* d_words = nullptr;   // static handles: status at [0], abort at [16], done at [32]
+  int32_t* d_words = nullptr;   // static handles: status at [0] (done record at [2..3]), abort at [16]
   void* last_stream = nullptr;
   bool launched = false;
-  uint32_t launch_seq = 0;      // launches enqueued so far
+  uint64_t last_done = 0;       // completion record the last launch writes (see DevModel::host_status)
   uint64_t timeout_ticks = 0;
   // the last kv_cache / logits pointers found to be device memory of this
   // device with room for a step's accesses (the check is skipped while the
@@ -123,7 +122,6 @@ void free_handle(amk_handle_s* h) {
   else if (h->d_block) (void)hipFree(h->d_block);
   if (h->h_status) (void)hipHostFree(h->h_status);
   if (h->h_abort) (void)hipHostFree(h->h_abort);
-  if (h->h_done) (void)hipHostFree(h->h_done);
   delete h;
 }
 
@@ -383,8 +381,8 @@ static int create_impl(const amk_config_t* cfg, const amk_weights_t* w, const am
     const Region r_argp = take(sizeof(float) * 2 * n_lm);
     const Region r_next = take(sizeof(int32_t));
     const Region r_abort = take(sizeof(int32_t));
-    // static handles: status, abort and done words, each on its own 64 bytes
-    const Region r_words = take(use_static ? 3 * 64 : 0);
+    // static handles: status (+ done record) and abort words, each on its own 64 bytes
+    const Region r_words = take(use_static ? 2 * 64 : 0);
     const bool tracing = tuning && tuning->trace;
     Region r_tasks[kVariants], r_queue[kVariants], r_trace[kVariants], r_ctr[kVariants];
     for (int v = 0; v < kVariants; ++v) {
@@ -427,28 +425,23 @@ static int create_impl(const amk_config_t* cfg, const amk_weights_t* w, const am
     }
     int32_t* d_status = nullptr;
     int32_t* d_hab = nullptr;
-    uint32_t* d_done = nullptr;
     if (use_static) {
       h->d_words = (int32_t*)(base + r_words.off);
       d_status = h->d_words;
       d_hab = h->d_words + 16;
-      d_done = (uint32_t*)(h->d_words + 32);
     } else {
-      if (hipHostMalloc((void**)&h->h_status, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+      // status word at [0], the 64-bit completion record at [2..3]
+      if (hipHostMalloc((void**)&h->h_status, 4 * sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
               hipSuccess ||
           hipHostMalloc((void**)&h->h_abort, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
-              hipSuccess ||
-          hipHostMalloc((void**)&h->h_done, sizeof(uint32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
               hipSuccess) {
         free_handle(h);
         return AMK_ERR_OUT_OF_MEMORY;
       }
-      *(volatile int32_t*)h->h_status = 0;
+      for (int i = 0; i < 4; ++i) ((volatile int32_t*)h->h_status)[i] = 0;
       *(volatile int32_t*)h->h_abort = 0;
-      *(volatile uint32_t*)h->h_done = 0;
       if (hipHostGetDevicePointer((void**)&d_status, h->h_status, 0) != hipSuccess ||
-          hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess ||
-          hipHostGetDevicePointer((void**)&d_done, h->h_done, 0) != hipSuccess) {
+          hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess) {
         free_handle(h);
         return AMK_ERR_DEVICE;
       }
@@ -522,7 +515,6 @@ static int create_impl(const amk_config_t* cfg, const amk_weights_t* w, const am
     m.dev_abort = (int32_t*)(base + r_abort.off);
     m.host_status = d_status;
     m.host_abort = d_hab;
-    m.host_done = d_done;
     for (int v = 0; v < kVariants; ++v) {
       h->dsch[v].tasks = (const amk_task_t*)(base + r_tasks[v].off);
       h->dsch[v].queue_start = (const int32_t*)(base + r_queue[v].off);
@@ -568,7 +560,8 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
     if (sticky != 0) return sticky;
     // another stream while the previous step has not finished: the two steps
     // would share the handle's counters and scratch
-    if (h->launched && stream != h->last_stream && *(volatile uint32_t*)h->h_done != h->launch_seq)
+    if (h->launched && stream != h->last_stream &&
+        __atomic_load_n((const uint64_t*)(h->h_status + 2), __ATOMIC_ACQUIRE) != h->last_done)
       return AMK_ERR_BAD_STATE;
   }
   DeviceGuard guard(h->device);
@@ -590,7 +583,6 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   m.queue_start = ds.queue_start;
   m.trace = ds.trace;
   m.counters = ds.counters;
-  m.launch_seq = h->launch_seq + 1;
   const uint32_t epoch = ds.epoch + 1;  // counter targets are epoch * producers, mod 2^32
   const int st = amk_internal_launch(&m, variant == AMK_SCHEDULE_TINY, token, pos, epoch, (uint16_t*)kv_cache, logits,
                                      h->timeout_ticks, stream);
@@ -599,7 +591,7 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   ds.epoch = epoch;
   h->last_stream = stream;
   h->launched = true;
-  h->launch_seq = m.launch_seq;
+  h->last_done = ((uint64_t)epoch << 32) | (uint32_t)(uintptr_t)ds.tasks;
   return AMK_OK;
 }
 
@@ -646,7 +638,8 @@ int amk_reset(amk_handle_t h) {
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
   if (!h->is_static) {
     *(volatile int32_t*)h->h_status = 0;
-    *(volatile uint32_t*)h->h_done = h->launch_seq;  // a stopped launch never reported its end
+    __atomic_store_n((uint64_t*)(h->h_status + 2), h->last_done, __ATOMIC_RELEASE);  // a stopped launch never
+                                                                                      // reported its end
   }
   return AMK_OK;
 }
