@@ -15,8 +15,12 @@ warm-ups and 100 timed steps; median and p10/p90 of the per-launch times are
 reported too).  Also reported: the whole-token host time including the
 next-token readback, the device's streaming-read peak (amk_read_probe over
 8 GiB), a flag for any time below the bandwidth floor, GPU clocks and power
-from amd-smi when it is present, and the CPU oracle's time per step (median
-of 3) on this host.
+from amd-smi when it is present (sampled by a background thread while the
+timed steps run), the CPU oracle's time per step (median of 3, weights
+decoded to fp32 before the timed region when host memory allows) on this
+host, and a same-node PyTorch-ROCm reference (per-op eager and HIP-graph
+replay of the same step, paper_2606_09682_amd.torch_baseline) for the bf16
+and W8A16 variants, itself checked against the oracle.
 """
 from __future__ import annotations
 
@@ -99,6 +103,41 @@ def smi_snapshot():
     return keep[:12] or None
 
 
+class SmiSampler:
+    """amd-smi snapshots taken by a background thread while the GPU works:
+    start() begins sampling, stop() ends it and returns the snapshots (the
+    caller keeps the GPU busy until enough were taken)."""
+
+    def __init__(self):
+        import threading
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = None
+
+    def start(self):
+        import threading
+        if smi_snapshot() is None:  # amd-smi absent
+            return self
+        self._thread = threading.Thread(target=self._run, daemon=True)
+        self._thread.start()
+        return self
+
+    def _run(self):
+        while not self._stop.is_set():
+            snap = smi_snapshot()
+            if snap:
+                self.samples.append({"t": round(time.perf_counter(), 3), "lines": snap})
+
+    def running(self):
+        return self._thread is not None and self._thread.is_alive()
+
+    def stop(self):
+        self._stop.set()
+        if self._thread is not None:
+            self._thread.join(timeout=30)
+        return self.samples
+
+
 def read_peak_gbs(amk, torch, nbytes=8 << 30):
     """Best streaming-read rate of this device over nbytes (amk_read_probe)."""
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -120,7 +159,7 @@ def read_peak_gbs(amk, torch, nbytes=8 << 30):
     return best
 
 
-def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repeats=1):
+def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repeats=1, baseline=True):
     import oracle
     import synth
     from synth.device import config_kwargs, kv_to_device, weights_to_device
@@ -139,19 +178,31 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repea
     res = {"fmt": fmt, "pos": pos}
     dec.step(1, pos, kv, logits)
     tok = dec.next_token()
+    ref_logits = None
     if check:
         log(f"variant {fmt} pos {pos}: oracle step")
-        model = oracle.OracleModel(w, fmt, np.float32, cache=False)
+        # the timed oracle (first variant) decodes its weights to fp32 before
+        # the timed region when host memory holds them twice over
+        upcast = oracle_repeats > 1 and host_free_bytes() > 3 * fp32_model_bytes(cfg)
+        model = oracle.OracleModel(w, fmt, np.float32, cache=upcast)
+        if upcast:
+            t0 = time.perf_counter()
+            for name in w.bf16:
+                if w.bf16[name].ndim == 2 and name != "embed" or (name == "embed" and cfg.tied_embeddings):
+                    model.mat(name)
+            log(f"oracle weights decoded to fp32 in {time.perf_counter() - t0:.1f}s (outside the timed region)")
         times = []
         for _ in range(oracle_repeats):
             kv_ref = kv_np.copy()
             t0 = time.perf_counter()
             ref_logits = oracle.decode_step(model, 1, pos, kv_ref)
             times.append(time.perf_counter() - t0)
+        del model
         cpu_s = float(np.median(times))
         ref_tok = oracle.argmax_first(ref_logits)
         err = float(np.max(np.abs(logits.cpu().numpy().astype(np.float64) - ref_logits)))
-        res.update(oracle_s=cpu_s, max_abs_logit_err=err, token=tok, oracle_token=ref_tok,
+        res.update(oracle_s=cpu_s, oracle_upcast=upcast, max_abs_logit_err=err, token=tok, oracle_token=ref_tok,
+                   oracle_top2_margin=oracle.top2_margin(ref_logits),
                    correct=bool(tok == ref_tok and err <= 2e-2))
         log(f"variant {fmt} pos {pos}: token {tok} oracle {ref_tok} err {err:.2e} oracle {cpu_s:.1f}s")
     else:
@@ -161,6 +212,7 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repea
         dec.step(1, pos, kv, logits)
     torch.cuda.synchronize()
     smi_before = smi_snapshot() if check else None
+    sampler = SmiSampler().start() if check else None
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     t0 = time.perf_counter()
@@ -171,6 +223,16 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repea
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     launch_us = np.array([s.elapsed_time(e) * 1e3 for s, e in zip(starts, ends)])
+    smi_during = []
+    if sampler is not None:
+        # the timed region is shorter than one amd-smi call: keep the same
+        # step running (untimed) until two samples were taken under load
+        t1 = time.perf_counter()
+        while sampler.running() and len(sampler.samples) < 2 and time.perf_counter() - t1 < 20:
+            for _ in range(20):
+                dec.step(1, pos, kv, logits)
+            torch.cuda.synchronize()
+        smi_during = sampler.stop()
     smi_after = smi_snapshot() if check else None
     # whole token as a host sees it: the API call plus the next-token readback
     n_rb = max(1, min(steps, 20))
@@ -181,6 +243,9 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repea
     token_wall_us = (time.perf_counter() - t0) / n_rb * 1e6
     status = dec.status()
     dec.close()
+    if baseline and fmt in ("bf16", "w8a16"):
+        res["torch_reference"] = torch_reference(torch, cfg, tensors, fmt, pos, kv_np, max_seq, steps, warmup,
+                                                 ref_logits)
     del tensors
     torch.cuda.empty_cache()
     nbytes = cfg.algorithmic_bytes(fmt, pos)
@@ -194,9 +259,67 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repea
     res["floor_ratio"] = res["launch_us_mean"] / res["floor_us"]
     # a time below the bandwidth floor would be a measurement artefact
     res["below_floor"] = bool(float(np.min(launch_us)) < res["floor_us"])
-    if smi_before or smi_after:
-        res["amd_smi"] = {"before": smi_before, "after": smi_after}
+    if smi_before or smi_after or smi_during:
+        res["amd_smi"] = {"before": smi_before, "during_load": smi_during, "after": smi_after}
     return res
+
+
+def host_free_bytes() -> int:
+    try:
+        import psutil
+        return int(psutil.virtual_memory().available)
+    except Exception:
+        return 0
+
+
+def fp32_model_bytes(cfg) -> int:
+    return 4 * (sum(o * i for _, o, i in cfg.linear_shapes()) * cfg.n_layers + cfg.vocab * cfg.hidden)
+
+
+def torch_reference(torch, cfg, tensors, fmt, pos, kv_np, max_seq, steps, warmup, ref_logits):
+    """The same step in plain PyTorch-ROCm, per-op eager and HIP-graph replay:
+    µs per token (step plus an on-device argmax), checked against the oracle's
+    logits when they were computed.  A same-node reference, not a target."""
+    from paper_2606_09682_amd import torch_baseline as tb
+    from synth.device import kv_to_device
+    log(f"variant {fmt} pos {pos}: torch reference")
+    ref = tb.TorchDecode(cfg, tensors, fmt, max_seq)
+    kv = kv_to_device(kv_np)
+    logits = torch.empty(cfg.vocab, dtype=torch.float32, device="cuda")
+    tok = torch.tensor([1], device="cuda")
+    ref.step(tok, pos, kv, logits)
+    out = {"kind": "pytorch-rocm per-op eager and HIP graph (bf16 GEMV via torch.nn.functional.linear)",
+           "weights_streamed": "bf16" if fmt == "bf16" else "bf16 (dequantised once from int8)"}
+    if ref_logits is not None:
+        err = float(np.max(np.abs(logits.cpu().numpy().astype(np.float64) - ref_logits)))
+        out.update(max_abs_logit_err=err, token=ref.next_token(logits),
+                   logit_bound=tb.logit_bound(ref_logits), oracle_top2_margin=float(
+                       np.partition(ref_logits, -2)[-1] - np.partition(ref_logits, -2)[-2]),
+                   correct=bool(err <= tb.logit_bound(ref_logits) and (
+                       ref.next_token(logits) == int(np.argmax(ref_logits)) or
+                       np.partition(ref_logits, -2)[-1] - np.partition(ref_logits, -2)[-2] <= 2 * err)))
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps
+
+    out["eager_us_per_token"] = timed(lambda: (ref.step(tok, pos, kv, logits), torch.argmax(logits)))
+    g = tb.GraphDecode(ref, pos, kv, logits)
+    out["graph_us_per_token"] = timed(lambda: (g.step(1), torch.argmax(logits)))
+    del g, ref
+    torch.cuda.empty_cache()
+    log(f"variant {fmt} pos {pos}: torch eager {out['eager_us_per_token']:.0f} us, "
+        f"graph {out['graph_us_per_token']:.0f} us")
+    return out
 
 
 def main():
@@ -208,6 +331,8 @@ def main():
     ap.add_argument("--variants", default="all",
                     help="'all', 'main' (bf16 at position 0 only) or a comma list of FMT@POS, e.g. w4a16@0")
     ap.add_argument("--no-check", action="store_true", help="skip the oracle gate (profiling runs)")
+    ap.add_argument("--no-torch-reference", action="store_true",
+                    help="skip the PyTorch-ROCm eager / HIP-graph reference (implied by --no-check)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
@@ -262,7 +387,8 @@ def main():
             synth.add_w4a16(w)
             log(f"quantised (int4, group {w.group4}) in {time.perf_counter() - t0:.1f}s")
         results.append(run_variant(amk, torch, w, fmt, pos, args.steps, args.warmup, check=not args.no_check,
-                                   oracle_repeats=3 if not results else 1))
+                                   oracle_repeats=3 if not results else 1,
+                                   baseline=not (args.no_check or args.no_torch_reference)))
         if results[-1].get("correct") is False or results[-1]["status"] != 0:
             log(f"variant {fmt} pos {pos} FAILED its correctness gate: {results[-1]}")
     main_res = results[0]
@@ -294,6 +420,7 @@ def main():
         "measured_read_peak_gbs": peak,
         "frac_of_measured_peak": (main_res["achieved_gbs"] / peak) if peak else None,
         "cpu_baseline": None,
+        "same_node_reference": main_res.get("torch_reference"),
         "variants": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in r.items()} for r in results],
     }
     if "oracle_s" in main_res:
@@ -301,8 +428,9 @@ def main():
         out["cpu_baseline"] = {"value": main_res["oracle_s"] * 1e6, "unit": "µs/token", "cores": threads,
                                "kind": "oracle",
                                "sample": f"median of 3 full decode steps of {workload} (numpy fp32, weights "
-                                         f"decoded from bf16 per use; BLAS {blas}, {os.cpu_count()} host "
-                                         f"CPUs, {host_ram_gb()} GiB RAM)"}
+                                         + ("decoded to fp32 before the timed region" if main_res.get("oracle_upcast")
+                                            else "decoded from bf16 per use (host memory too small to hold fp32)")
+                                         + f"; BLAS {blas}, {os.cpu_count()} host CPUs, {host_ram_gb()} GiB RAM)"}
     print(json.dumps(out), flush=True)
 
 
