@@ -179,9 +179,10 @@ int amk_create(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning
  * earlier step (AMK_ERR_TIMEOUT / AMK_ERR_ABORTED / AMK_ERR_NONFINITE,
  * visible once that step finished) is returned and nothing is launched until
  * amk_reset().  One handle must not be driven from two streams at once: a
- * step enqueued on a different stream than the previous one while that
- * stream still has work pending returns AMK_ERR_BAD_STATE and launches
- * nothing (synchronise the old stream before switching). */
+ * step enqueued on a different stream than the previous step's while that
+ * stream still has work queued (the previous step, or anything after it)
+ * returns AMK_ERR_BAD_STATE and launches nothing (synchronise the old stream
+ * before switching). */
 int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, float* logits,
                     void* stream);
 
@@ -211,9 +212,8 @@ int amk_destroy(amk_handle_t h);
  * two handles would race on the same counters and scratch).  Because the
  * status words are device memory, amk_decode_step on a static handle does not
  * return an earlier step's sticky error (amk_get_status, which waits for the
- * stream, does), does not detect use from two streams, and amk_set_abort
- * returns AMK_ERR_UNSUPPORTED; every counter wait is still bounded by the
- * deadline.  amk_destroy and every other function work as for amk_create. */
+ * stream, does) and amk_set_abort returns AMK_ERR_UNSUPPORTED; every counter
+ * wait is still bounded by the deadline.  amk_destroy and every other function work as for amk_create. */
 int amk_create_static(const amk_config_t* cfg, const amk_weights_t* w, const amk_tuning_t* tuning,
                       amk_handle_t* out);
 

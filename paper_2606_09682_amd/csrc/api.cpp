@@ -56,10 +56,9 @@ struct amk_handle_s {
   // amk_create_static: the device block is the library's static scratch
   // array, and the status / abort / done words are device words in it
   bool is_static = false;
-  int32_t* d_words = nullptr;   // static handles: status at [0] (done record at [2..3]), abort at [16]
+  int32_t* d_words = nullptr;   // static handles: status at [0], abort at [16]
   void* last_stream = nullptr;
   bool launched = false;
-  uint64_t last_done = 0;       // completion record the last launch writes (see DevModel::host_status)
   uint64_t timeout_ticks = 0;
   // the last kv_cache / logits pointers found to be device memory of this
   // device with room for a step's accesses (the check is skipped while the
@@ -381,7 +380,7 @@ static int create_impl(const amk_config_t* cfg, const amk_weights_t* w, const am
     const Region r_argp = take(sizeof(float) * 2 * n_lm);
     const Region r_next = take(sizeof(int32_t));
     const Region r_abort = take(sizeof(int32_t));
-    // static handles: status (+ done record) and abort words, each on its own 64 bytes
+    // static handles: status and abort words, each on its own 64 bytes
     const Region r_words = take(use_static ? 2 * 64 : 0);
     const bool tracing = tuning && tuning->trace;
     Region r_tasks[kVariants], r_queue[kVariants], r_trace[kVariants], r_ctr[kVariants];
@@ -430,15 +429,14 @@ static int create_impl(const amk_config_t* cfg, const amk_weights_t* w, const am
       d_status = h->d_words;
       d_hab = h->d_words + 16;
     } else {
-      // status word at [0], the 64-bit completion record at [2..3]
-      if (hipHostMalloc((void**)&h->h_status, 4 * sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+      if (hipHostMalloc((void**)&h->h_status, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
               hipSuccess ||
           hipHostMalloc((void**)&h->h_abort, sizeof(int32_t), hipHostMallocMapped | hipHostMallocCoherent) !=
               hipSuccess) {
         free_handle(h);
         return AMK_ERR_OUT_OF_MEMORY;
       }
-      for (int i = 0; i < 4; ++i) ((volatile int32_t*)h->h_status)[i] = 0;
+      *(volatile int32_t*)h->h_status = 0;
       *(volatile int32_t*)h->h_abort = 0;
       if (hipHostGetDevicePointer((void**)&d_status, h->h_status, 0) != hipSuccess ||
           hipHostGetDevicePointer((void**)&d_hab, h->h_abort, 0) != hipSuccess) {
@@ -553,19 +551,23 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   if (!h || !kv_cache || !logits) return AMK_ERR_INVALID_ARGUMENT;
   if (token < 0 || token >= h->s.V || pos < 0 || pos >= h->s.max_seq) return AMK_ERR_INVALID_ARGUMENT;
   if (((uintptr_t)kv_cache & 255u) != 0 || !aligned16(logits)) return AMK_ERR_INVALID_ARGUMENT;
-  // (a static handle's status words are device memory: reading them would
-  // wait for the device, so neither check is made for it)
+  // (a static handle's status word is device memory: reading it would wait
+  // for the device, so the sticky check is not made for it)
   if (!h->is_static) {
     const int sticky = *(volatile int32_t*)h->h_status;
     if (sticky != 0) return sticky;
-    // another stream while the previous step has not finished: the two steps
-    // would share the handle's counters and scratch
-    if (h->launched && stream != h->last_stream &&
-        __atomic_load_n((const uint64_t*)(h->h_status + 2), __ATOMIC_ACQUIRE) != h->last_done)
-      return AMK_ERR_BAD_STATE;
   }
   DeviceGuard guard(h->device);
   if (!guard.ok) return AMK_ERR_DEVICE;
+  // another stream while the previous one still has work queued (which may
+  // be this handle's last step): two steps would share the handle's
+  // counters and scratch.  A stream that no longer exists reports an error
+  // here, not pending work.
+  if (h->launched && stream != h->last_stream) {
+    const hipError_t q = hipStreamQuery((hipStream_t)h->last_stream);
+    if (q != hipSuccess) (void)hipGetLastError();
+    if (q == hipErrorNotReady) return AMK_ERR_BAD_STATE;
+  }
   if (kv_cache != h->ok_kv) {
     if (!device_range(kv_cache, amk_kv_cache_bytes_of(h->s), h->device)) return AMK_ERR_INVALID_ARGUMENT;
     h->ok_kv = kv_cache;
@@ -591,7 +593,6 @@ int amk_decode_step(amk_handle_t h, int32_t token, int32_t pos, void* kv_cache, 
   ds.epoch = epoch;
   h->last_stream = stream;
   h->launched = true;
-  h->last_done = ((uint64_t)epoch << 32) | (uint32_t)(uintptr_t)ds.tasks;
   return AMK_OK;
 }
 
@@ -638,8 +639,6 @@ int amk_reset(amk_handle_t h) {
   if (hipDeviceSynchronize() != hipSuccess) return AMK_ERR_DEVICE;
   if (!h->is_static) {
     *(volatile int32_t*)h->h_status = 0;
-    __atomic_store_n((uint64_t*)(h->h_status + 2), h->last_done, __ATOMIC_RELEASE);  // a stopped launch never
-                                                                                      // reported its end
   }
   return AMK_OK;
 }

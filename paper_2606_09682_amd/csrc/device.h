@@ -66,9 +66,7 @@ struct DevModel {
   int32_t* next_token;       // [1]
   uint32_t* counters;        // [n_counters * kCounterReplicas * kCounterStride]
   int32_t* dev_abort;        // device word: nonzero stops every workgroup at its next wait
-  int32_t* host_status;      // host-mapped: [0] first device error code; [2..3] as one uint64,
-                             // (epoch << 32) | low 32 bits of `tasks` of the last launch whose
-                             // argmax finished
+  int32_t* host_status;      // host-mapped: first device error code
   const int32_t* host_abort; // host-mapped: raised by amk_set_abort
   // schedule of this launch (one of the handle's variants)
   uint64_t* trace;           // [n_tasks][AMK_TRACE_FIELDS] timestamps, or null

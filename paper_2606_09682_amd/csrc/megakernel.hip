@@ -870,13 +870,7 @@ __device__ __forceinline__ void epi_lmhead(const DevModel& m, const amk_task_t& 
   if (lane == 0) stc(reinterpret_cast<float2*>(m.argp + 2 * t.aux), make_float2(best, __int_as_float(besti)));
 }
 
-// The step's completion record: this launch's epoch and the low 32 bits of
-// its task table (which names the schedule variant), in one 64-bit word.
-__device__ __forceinline__ uint64_t done_record(const DevModel& m, uint32_t epoch) {
-  return ((uint64_t)epoch << 32) | (uint32_t)(uintptr_t)m.tasks;
-}
-
-__device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t& t, uint32_t epoch, int lane) {
+__device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t& t, int lane) {
   float best = -INFINITY;
   int besti = 0x7fffffff;
   for (int s = t.begin + lane; s < t.end; s += 64) {
@@ -890,12 +884,7 @@ __device__ __forceinline__ void argmax_final(const DevModel& m, const amk_task_t
     const int oi = __shfl_xor(besti, o);
     if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
   }
-  if (lane == 0) {
-    stc(m.next_token, besti);
-    // every other task of the step happens before this one: the step is done
-    __hip_atomic_store(reinterpret_cast<uint64_t*>(m.host_status + 2), done_record(m, epoch), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_SYSTEM);
-  }
+  if (lane == 0) stc(m.next_token, besti);
 }
 
 // ---------------------------------------------------------------- attention (all 8 waves)
@@ -1462,7 +1451,7 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
         case AMK_OP_O: case AMK_OP_DOWN: epi_residual(m, t, g, L, ctl, lane); break;
         case AMK_OP_GATEUP: epi_gateup(m, t, g, L, input_rs(m, ctl), lane); break;
         case AMK_OP_LMHEAD: epi_lmhead(m, t, g, L, input_rs(m, ctl), logits, lane); break;
-        case AMK_OP_ARGMAX: argmax_final(m, t, epoch, lane); break;
+        case AMK_OP_ARGMAX: argmax_final(m, t, lane); break;
         default: break;
       }
       if (tr && lane == 0) stg<uint64_t>(tr + AMK_TRACE_PUBLISHED, (uint64_t)wall_clock64());
