@@ -447,24 +447,15 @@ __device__ __forceinline__ float dot_gran(const uint4 v, const float* __restrict
 // One int4 granule: the lane's 32 columns [c * 2048 + 32 lane, + 32) of one
 // row, times their group scale s.  Word d of the lane's 16 bytes holds
 // columns 8d .. 8d + 3 in its low nibbles and 8d + 4 .. 8d + 7 in its high
-// nibbles, as unsigned code + 8: masking gives four byte-sized values each,
-// which convert to float one byte at a time (the high ones come out times 16,
-// an exact power of two taken out once).  The zero point leaves
-// sum (code + 8) x - 8 sum x, with sum x over the 32 columns precomputed.
-__device__ __forceinline__ float ub(uint32_t w, int k) { return (float)((w >> (8 * k)) & 0xffu); }
-// w & mask, opaque to the optimiser: with the mask visible it rewrites each
-// byte conversion of the masked word as a bit-field extract plus a
-// conversion, two VALU ops per nibble instead of one v_cvt_f32_ubyteN.
-__device__ __forceinline__ uint32_t low_nibbles(uint32_t w) {
-  uint32_t r;
-  asm("v_and_b32 %0, 0x0f0f0f0f, %1" : "=v"(r) : "v"(w));
-  return r;
-}
-__device__ __forceinline__ uint32_t high_nibbles(uint32_t w) {
-  uint32_t r;
-  asm("v_and_b32 %0, 0xf0f0f0f0, %1" : "=v"(r) : "v"(w));
-  return r;
-}
+// nibbles, as unsigned code + 8.  Masked (and the high ones shifted down)
+// into the low nibble of each byte, a byte n read as an FP8 E4M3 value
+// (exponent field 0 or 1, bias 7) is exactly n * 2^-9, so one
+// v_cvt_pk_f32_fp8 turns two nibbles into floats.  Every product and partial
+// sum then carries the exact factor 2^-9, which rounding commutes with, so
+// the sum equals the plain fp32 one bit for bit once the factor is taken
+// out.  The zero point leaves sum (code + 8) x - 8 sum x, with sum x over the
+// 32 columns precomputed.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float dot_gran4(const uint4 v, uint32_t sbits, const float* __restrict__ act,
                                            const float* __restrict__ xsum, int c, int lane, bool valid, float acc) {
   const float* x = act + act_gran<GRAN4>(c, lane * LANE4);
@@ -474,13 +465,15 @@ __device__ __forceinline__ float dot_gran4(const uint4 v, uint32_t sbits, const 
   for (int d = 0; d < 4; ++d) {
     const float4 a = *reinterpret_cast<const float4*>(x + 8 * d);
     const float4 b = *reinterpret_cast<const float4*>(x + 8 * d + 4);
-    const uint32_t l = low_nibbles(w[d]), h = high_nibbles(w[d]);
-    lo = fmaf(ub(l, 0), a.x, lo); lo = fmaf(ub(l, 1), a.y, lo);
-    lo = fmaf(ub(l, 2), a.z, lo); lo = fmaf(ub(l, 3), a.w, lo);
-    hi = fmaf(ub(h, 0), b.x, hi); hi = fmaf(ub(h, 1), b.y, hi);
-    hi = fmaf(ub(h, 2), b.z, hi); hi = fmaf(ub(h, 3), b.w, hi);
+    const int l = (int)(w[d] & 0x0f0f0f0fu), h = (int)((w[d] >> 4) & 0x0f0f0f0fu);
+    const f32x2 l01 = __builtin_amdgcn_cvt_pk_f32_fp8(l, false), l23 = __builtin_amdgcn_cvt_pk_f32_fp8(l, true);
+    const f32x2 h01 = __builtin_amdgcn_cvt_pk_f32_fp8(h, false), h23 = __builtin_amdgcn_cvt_pk_f32_fp8(h, true);
+    lo = fmaf(l01.x, a.x, lo); lo = fmaf(l01.y, a.y, lo);
+    lo = fmaf(l23.x, a.z, lo); lo = fmaf(l23.y, a.w, lo);
+    hi = fmaf(h01.x, b.x, hi); hi = fmaf(h01.y, b.y, hi);
+    hi = fmaf(h23.x, b.z, hi); hi = fmaf(h23.y, b.w, hi);
   }
-  const float u = fmaf(hi, 0.0625f, lo);                       // sum of (code + 8) x
+  const float u = (lo + hi) * 512.f;                             // sum of (code + 8) x
   const float p = fmaf(-8.f, xsum[c * (GRAN4 / LANE4) + lane], u);  // sum of code x
   const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)sbits);
   return valid ? fmaf(s, p, acc) : acc;
