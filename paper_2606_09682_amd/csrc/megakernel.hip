@@ -460,11 +460,16 @@ __device__ __forceinline__ float dot_gran4(const uint4 v, uint32_t sbits, const 
                                            const float* __restrict__ xsum, int c, int lane, bool valid, float acc) {
   const float* x = act + act_gran<GRAN4>(c, lane * LANE4);
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  // all 32 activations and their sum are read before any product, so the
+  // LDS latency is paid once per granule
+  float4 xv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) xv[i] = *reinterpret_cast<const float4*>(x + 4 * i);
+  const float xs = xsum[c * (GRAN4 / LANE4) + lane];
   float lo = 0.f, hi = 0.f;
 #pragma unroll
   for (int d = 0; d < 4; ++d) {
-    const float4 a = *reinterpret_cast<const float4*>(x + 8 * d);
-    const float4 b = *reinterpret_cast<const float4*>(x + 8 * d + 4);
+    const float4 a = xv[2 * d], b = xv[2 * d + 1];
     const int l = (int)(w[d] & 0x0f0f0f0fu), h = (int)((w[d] >> 4) & 0x0f0f0f0fu);
     const f32x2 l01 = __builtin_amdgcn_cvt_pk_f32_fp8(l, false), l23 = __builtin_amdgcn_cvt_pk_f32_fp8(l, true);
     const f32x2 h01 = __builtin_amdgcn_cvt_pk_f32_fp8(h, false), h23 = __builtin_amdgcn_cvt_pk_f32_fp8(h, true);
@@ -474,7 +479,7 @@ __device__ __forceinline__ float dot_gran4(const uint4 v, uint32_t sbits, const 
     hi = fmaf(h23.x, b.z, hi); hi = fmaf(h23.y, b.w, hi);
   }
   const float u = (lo + hi) * 512.f;                             // sum of (code + 8) x
-  const float p = fmaf(-8.f, xsum[c * (GRAN4 / LANE4) + lane], u);  // sum of code x
+  const float p = fmaf(-8.f, xs, u);                             // sum of code x
   const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)sbits);
   return valid ? fmaf(s, p, acc) : acc;
 }
