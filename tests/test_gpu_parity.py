@@ -131,11 +131,23 @@ def compare(name, fmt, g, o, pos0):
     # layer 0 of the first step sees bit-identical inputs on both sides: one bf16 step
     bound = np.maximum(np.abs(a[0, :, :, 0]), np.abs(b[0, :, :, 0])) * 2.0 ** -7 + 1e-5
     assert np.all(np.abs(a[0, :, :, 0] - b[0, :, :, 0]) <= bound)
-    # deeper layers inherit earlier rounding flips: relative L2 error per layer and K/V
+    # deeper layers inherit earlier rounding flips: relative L2 error per layer and K/V, and
+    # every element within one bf16 step of the oracle's plus the hidden-state difference
+    # carried from earlier layers and steps.  That difference comes from one-step bf16
+    # flips of earlier K/V elements (at pos 0 the attention output is the V row itself, so
+    # a flip passes straight into the residual stream) and fp32 reassociation: measured up
+    # to 6.7e-3 of the layer's RMS (32-step SmolLM2 W8A16 decode; 5.5e-3 in one 8B step);
+    # bounded by 2e-2, while a misplaced or wrong element is off by about the RMS itself
+    worst = 0.0
     for l in range(a.shape[0]):
         for t in range(2):
             rel = np.linalg.norm(a[l, t] - b[l, t]) / max(np.linalg.norm(b[l, t]), 1e-30)
             assert rel <= 1e-2, (l, t, rel)
+            rms = float(np.sqrt(np.mean(b[l, t] ** 2)))
+            excess = np.abs(a[l, t] - b[l, t]) - np.maximum(np.abs(a[l, t]), np.abs(b[l, t])) * 2.0 ** -7
+            worst = max(worst, float(np.max(excess)) / max(rms, 1e-30))
+    say(f"{name} {fmt}: appended K/V rows, largest excess over one bf16 step = {worst:.2e} of the layer RMS")
+    assert worst <= 2e-2, worst
     # untouched slots are left alone
     mask = np.ones(g_kv.shape[3], bool)
     mask[sl] = False
