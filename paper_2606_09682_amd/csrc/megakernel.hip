@@ -29,7 +29,7 @@
 // workgroup meets at B4, the sync wave releases and signals the chain
 // counter, and B5 keeps the next task's weight loads behind that signal.
 // The streaming waves issue the weight loads of their NEXT task right after
-// B3.  Memory requests of one CU are served roughly in order, so loads issued
+// B3 (int4 weights in the tiny-context kernel: right after B2).  Memory requests of one CU are served roughly in order, so loads issued
 // before the result stores, the release or the counter increment would delay
 // every consumer on other CUs; issued after them, the loads stream while the
 // counters propagate and the next input is fetched.  The pipeline is kept
@@ -1440,6 +1440,15 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
       }
     }
     __syncthreads();  // B2: GEMV partials in LDS, attention results stored
+    // W4A16 in the tiny-context kernel: the next task's weight loads go out now,
+    // while the sync wave publishes.  They delay this task's result stores in
+    // the CU's request queue, which measured slower for bf16 and int8 weights
+    // (+23 us per 8B step each) and faster for int4 (-34 us), whose tasks carry
+    // a quarter of bf16's bytes per row.
+    constexpr bool EARLY = TINY && FMT == AMK_WEIGHTS_W4A16;
+    if constexpr (EARLY) {
+      if (wave != 0) prefetch(idx + 1);
+    }
 
     // ---- publish (sync wave)
     if (wave == 0) {
@@ -1492,7 +1501,9 @@ amk_decode_kernel(DevModel m, int32_t token, int32_t pos, uint32_t epoch, uint16
     }
 
     // ---- the next task's weight stream (streaming waves)
-    if (wave != 0) prefetch(idx + 1);
+    if constexpr (!EARLY) {
+      if (wave != 0) prefetch(idx + 1);
+    }
   }
 }
 
