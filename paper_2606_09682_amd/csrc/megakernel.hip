@@ -29,9 +29,10 @@
 // workgroup meets at B4, the sync wave releases and signals the chain
 // counter, and B5 keeps the next task's weight loads behind that signal.
 // The streaming waves issue the weight loads of their NEXT task right after
-// B3 (int4 weights in the tiny-context kernel: right after B2).  Memory requests of one CU are served roughly in order, so loads issued
-// before the result stores, the release or the counter increment would delay
-// every consumer on other CUs; issued after them, the loads stream while the
+// B3 (int4 weights in the tiny-context kernel: right after B2).  Memory
+// requests of one CU are served roughly in order, so loads issued before the
+// result stores, the release or the counter increment would delay every
+// consumer on other CUs; issued after them, the loads stream while the
 // counters propagate and the next input is fetched.  The pipeline is kept
 // shallow (two halves of Pipe<FMT>::N granules per wave): measured on the
 // Llama-3-8B shape, deeper pipelines both delay the sync wave's polls and
