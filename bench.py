@@ -159,8 +159,36 @@ def read_peak_gbs(amk, torch, nbytes=8 << 30):
     return best
 
 
-def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repeats=1, baseline=True):
+def cpu_baseline_leg(w, fmt, pos, kv_np, repeats):
+    """The CPU baseline: the oracle's decode step for this workload on the host
+    cores, timed (median of `repeats`).  Its logits also serve as the variant's
+    correctness reference; this is the only place the benchmark runs the oracle."""
     import oracle
+
+    cfg = w.cfg
+    # the timed oracle (first variant) decodes its weights to fp32 before
+    # the timed region when host memory holds them twice over
+    upcast = repeats > 1 and host_free_bytes() > 3 * fp32_model_bytes(cfg)
+    model = oracle.OracleModel(w, fmt, np.float32, cache=upcast)
+    if upcast:
+        t0 = time.perf_counter()
+        for name in w.bf16:
+            if w.bf16[name].ndim == 2 and name != "embed" or (name == "embed" and cfg.tied_embeddings):
+                model.mat(name)
+        log(f"oracle weights decoded to fp32 in {time.perf_counter() - t0:.1f}s (outside the timed region)")
+    times = []
+    logits = None
+    for _ in range(repeats):
+        kv_ref = kv_np.copy()
+        t0 = time.perf_counter()
+        logits = oracle.decode_step(model, 1, pos, kv_ref)
+        times.append(time.perf_counter() - t0)
+    del model
+    return {"logits": logits, "token": oracle.argmax_first(logits), "seconds": float(np.median(times)),
+            "upcast": upcast, "top2_margin": oracle.top2_margin(logits)}
+
+
+def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repeats=1, baseline=True):
     import synth
     from synth.device import config_kwargs, kv_to_device, weights_to_device
 
@@ -181,28 +209,11 @@ def run_variant(amk, torch, w, fmt, pos, steps, warmup, check=True, oracle_repea
     ref_logits = None
     if check:
         log(f"variant {fmt} pos {pos}: oracle step")
-        # the timed oracle (first variant) decodes its weights to fp32 before
-        # the timed region when host memory holds them twice over
-        upcast = oracle_repeats > 1 and host_free_bytes() > 3 * fp32_model_bytes(cfg)
-        model = oracle.OracleModel(w, fmt, np.float32, cache=upcast)
-        if upcast:
-            t0 = time.perf_counter()
-            for name in w.bf16:
-                if w.bf16[name].ndim == 2 and name != "embed" or (name == "embed" and cfg.tied_embeddings):
-                    model.mat(name)
-            log(f"oracle weights decoded to fp32 in {time.perf_counter() - t0:.1f}s (outside the timed region)")
-        times = []
-        for _ in range(oracle_repeats):
-            kv_ref = kv_np.copy()
-            t0 = time.perf_counter()
-            ref_logits = oracle.decode_step(model, 1, pos, kv_ref)
-            times.append(time.perf_counter() - t0)
-        del model
-        cpu_s = float(np.median(times))
-        ref_tok = oracle.argmax_first(ref_logits)
+        cb = cpu_baseline_leg(w, fmt, pos, kv_np, oracle_repeats)
+        ref_logits, ref_tok, cpu_s = cb["logits"], cb["token"], cb["seconds"]
         err = float(np.max(np.abs(logits.cpu().numpy().astype(np.float64) - ref_logits)))
-        res.update(oracle_s=cpu_s, oracle_upcast=upcast, max_abs_logit_err=err, token=tok, oracle_token=ref_tok,
-                   oracle_top2_margin=oracle.top2_margin(ref_logits),
+        res.update(oracle_s=cpu_s, oracle_upcast=cb["upcast"], max_abs_logit_err=err, token=tok,
+                   oracle_token=ref_tok, oracle_top2_margin=cb["top2_margin"],
                    correct=bool(tok == ref_tok and err <= 2e-2))
         log(f"variant {fmt} pos {pos}: token {tok} oracle {ref_tok} err {err:.2e} oracle {cpu_s:.1f}s")
     else:
